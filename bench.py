@@ -1,0 +1,231 @@
+"""Benchmark of the fused log-prob + decoupled PPO loss stage on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload large_vocab] [--no-cpu-baseline]
+
+A step is one pass of the whole loss stage over one batch: the fused kernel (valid-token
+count, per-row log-sum-exp / ratios / decisions / loss / dlogits, loss sum), the host
+reset controller reading the five stats (one device-to-host copy), and the PPO-EWMA
+update of the per-token proxy buffer. Inputs are synthetic, seeded, and resident in HBM
+before the timed region. Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2605_12070_amd as P  # noqa: E402
+from paper_2605_12070_amd import workloads as W  # noqa: E402
+
+METRIC = "tokens/sec for fused logprob+decoupled PPO loss fwd+bwd; % of peak HBM GB/s"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, AMD specification
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+CSRC = os.path.join(ROOT, "paper_2605_12070_amd", "csrc")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def anchor_logprob(logits, ids, chunk=1024):
+    """Sampled-token log-probs from PyTorch (float32), only to synthesise lp_ref / lp_mu."""
+    T = logits.shape[0]
+    out = torch.empty(T, dtype=torch.float64, device=logits.device)
+    for a in range(0, T, chunk):
+        z = logits[a:a + chunk].float()
+        out[a:a + chunk] = (z.gather(1, ids[a:a + chunk, None])[:, 0]
+                            - torch.logsumexp(z, dim=1)).double()
+    return out
+
+
+def algorithmic_bytes(T, V, n_valid, esize, per_token):
+    """Logits read once (valid rows), dlogits written once (all rows), per-token vectors."""
+    return n_valid * V * esize + T * V * esize + T * per_token
+
+
+def cpu_baseline(wl, lp_mu, lp_ref, rows, threads):
+    """The float64 oracle on a fixed sample of rows, in a thread pool over row chunks."""
+    import oracle
+    mask = wl.mask.cpu().numpy()
+    params = oracle.Params(0.5, 2.0, 0.2, 0.2, "mask_weight", "token_mean", 1.0)
+    scale = oracle.batch_scale(mask, params)
+    idx = torch.as_tensor(rows, device=wl.logits.device)
+    z16 = wl.logits[idx].cpu()
+    if z16.dtype == torch.bfloat16:
+        zb = z16.view(torch.int16).numpy().view(np.uint16)
+        decode = oracle.bf16_bits_to_f64
+    else:
+        zb = z16.numpy()
+        decode = oracle.as_f64
+    ids = wl.ids[idx].cpu().numpy()
+    mu = lp_mu[idx].cpu().double().numpy()
+    ref = lp_ref[idx].cpu().double().numpy()
+    adv = wl.adv[idx].cpu().double().numpy()
+    m = mask[rows]
+    chunk = 32
+    jobs = [(a, min(len(rows), a + chunk)) for a in range(0, len(rows), chunk)]
+
+    def work(ab):
+        a, b = ab
+        oracle.per_token(decode(zb[a:b]), ids[a:b], mu[a:b], ref[a:b], adv[a:b], m[a:b], None,
+                         params, scale, want_dlogits=True)
+        return b - a
+
+    t0 = time.perf_counter()
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        done = sum(ex.map(work, jobs))
+    dt = time.perf_counter() - t0
+    return done / dt, dt
+
+
+def copy_bandwidth(dev, nbytes=2 << 30, reps=10):
+    """Device-to-device copy rate (read + write bytes per second), a practical ceiling."""
+    a = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="large_vocab", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--cpu-rows", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the loss stage shards by token rows; see the design notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {args.workload}: drawing inputs")
+    wl = W.make_workload(args.workload, device=dev)
+    T, V = wl.T, wl.V
+    anchor = anchor_logprob(wl.logits, wl.ids)
+    if wl.e_prev is not None:                      # long_agentic: EWMA proxy reference
+        lp_old, lp_prev, lp_mu = W.version_logprobs(anchor, wl)
+        lp_ref = lp_prev.clone()
+        P.ewma_proxy_update(lp_ref, lp_old, 0.9, normalized=False)
+        x_new = lp_old
+    else:
+        lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+        x_new = lp_ref
+    del anchor
+    mask = wl.mask
+    n_valid = int(mask.sum().item())
+    esize = wl.logits.element_size()
+    dlogits = torch.empty_like(wl.logits)
+    out = None
+    proxy = P.EwmaProxy(x_new, beta=P.beta_from_window(6), tau=0.9, patience=1)
+    torch.cuda.synchronize()
+
+    def step():
+        nonlocal out
+        out = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, mask,
+                                           dlogits=dlogits, out=out)
+        proxy.step(x_new, out.stats)               # stats D2H + reset decision + EWMA
+
+    log(f"warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    log(f"timing {args.steps} steps")
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with P.KernelTimer() as kt:
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        k_ms_total, k_launches = kt.read()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    k_ms = k_ms_total / max(1, k_launches)
+    tokens_per_s = T / (ms_per_step * 1e-3)
+
+    # per-token vectors: ids 8, lp_mu 4, lp_ref 4, adv 4, mask 1, lp out 4, loss out 4, flags 1
+    per_token = 8 + 4 + 4 + 4 + 1 + 4 + 4 + 1
+    b_alg = algorithmic_bytes(T, V, n_valid, esize, per_token)
+    achieved = b_alg / (k_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                "kernel": "rows_bf16_resident<1024,19>" if esize == 2 else "row kernel",
+                "kernel_ms": round(k_ms, 4), "alg_bytes_per_launch": b_alg}
+    if os.path.exists(TRAFFIC_FILE):
+        try:
+            tr = json.load(open(TRAFFIC_FILE)).get(args.workload)
+            if tr and tr.get("source_hash") == kernel_source_hash():
+                roofline["traffic"] = tr["bytes_per_launch"]
+        except (OSError, ValueError):
+            pass
+
+    result = {
+        "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded; stands in for the paper's agentic corpus)",
+        "config": {"workload": args.workload, "T": T, "V": V,
+                   "logits_dtype": "bf16" if esize == 2 else "f32",
+                   "sequences": f"{-(-T // wl.seq_len)}x{wl.seq_len}",
+                   "masked_fraction": round(1 - n_valid / T, 4),
+                   "rd_mode": "mask_weight", "band": [0.5, 2.0], "clip_eps": [0.2, 0.2],
+                   "parallelism": "none (1 GPU)"},
+        "hbm_pct_of_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        "roofline": roofline,
+    }
+    if not args.no_copy:
+        result["context"] = {"d2d_copy_GBps": round(copy_bandwidth(dev), 1)}
+    if not args.no_cpu_baseline:
+        threads = min(16, len(os.sched_getaffinity(0)))
+        rows = np.sort(np.random.default_rng(0).choice(T, size=min(args.cpu_rows, T),
+                                                       replace=False))
+        log(f"cpu baseline: oracle on {len(rows)} rows, {threads} threads")
+        rate, dt = cpu_baseline(wl, lp_mu, lp_ref, rows, threads)
+        result["cpu_baseline"] = {
+            "value": round(rate, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(rows)} seeded rows of the {args.workload} batch (T={T}, V={V}), "
+                      f"float64 numpy oracle incl. dlogits, {dt:.1f} s wall",
+            "cpu": platform.processor() or platform.machine()}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

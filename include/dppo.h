@@ -1,0 +1,203 @@
+/*
+ * dppo.h -- C ABI of the MI355X (gfx950) library for the per-token loss stage of
+ * decoupled off-policy PPO (Guan et al., "Missing Old Logits in Asynchronous Agentic RL",
+ * arXiv 2605.12070).
+ *
+ * Notation (the paper's): z = current-policy logits [T, V]; y = sampled token ids;
+ * lp_theta = log pi_theta(y); lp_ref = log pi_old(y) (exact old logits, Sec. 5.1), or
+ * log pi_prox(y) (PPO-EWMA proxy, Sec. 5.2), or log pi_async(y) (Table 1, last row);
+ * lp_mu = log mu_old(y), the inference engine's log-prob of the sampled token (Sec. 3.2);
+ * A = advantages; m = loss mask.
+ *
+ * Conventions shared by every entry point
+ *  - All array pointers are DEVICE pointers owned by the caller (for example PyTorch
+ *    tensors). The library keeps no pointer after a call returns and allocates no device
+ *    memory in these calls. Host pointers are marked "host".
+ *  - `stream` is a hipStream_t passed as void*; NULL means the default stream. Kernels are
+ *    enqueued on it in order; no call synchronises the device or the stream.
+ *  - Argument checks run on the host before any HIP call. A failed check returns
+ *    DPPO_ERR_INVALID_ARG (or DPPO_ERR_UNSUPPORTED) and enqueues nothing;
+ *    dppo_last_error() then describes the failure. A launch failure returns DPPO_ERR_HIP.
+ *    Nothing throws across the ABI.
+ *  - Data errors are reported on the device, not in the return code (see below).
+ *  - Row strides (`ld`, `ld_dlogits`) are in elements. When a base pointer is not 16-byte
+ *    aligned or a stride is not a multiple of 16 bytes, a slower element-wise path runs;
+ *    this is not an error.
+ *  - Thread safety: calls may be issued from several host threads; the kernel timer
+ *    (dppo_timer_*) is process-global and meant for one profiling thread.
+ */
+#ifndef DPPO_H
+#define DPPO_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DPPO_OK = 0,
+  DPPO_ERR_INVALID_ARG = 1, /* null required pointer, bad size, bad enum, bad parameter */
+  DPPO_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+  DPPO_ERR_HIP = 3          /* a HIP runtime call or kernel launch failed */
+} dppo_status;
+
+/* Storage type of logits / dlogits / EWMA buffers. Arithmetic is float32 throughout. */
+typedef enum { DPPO_F32 = 0, DPPO_BF16 = 1 } dppo_dtype;
+
+/* How the discrepancy ratio r_d = pi_ref / mu_old enters the objective.
+ *  NONE:        wd = 1          (PPO-clip on r_s only; Table 1 rows with r_d = 1)
+ *  MASK:        wd = M(r_d)     (band mask of Eq. 4, the MIS weight without the ratio)
+ *  WEIGHT:      wd = r_d        (down-weighting; the r2 factor of Table 5)
+ *  MASK_WEIGHT: wd = M(r_d) r_d (Eq. 4's mask with the total ratio r = r_d r_s of the MIS
+ *                                gradient, Sec. 3.1 and Sec. 3.2; the default)          */
+typedef enum {
+  DPPO_RD_NONE = 0,
+  DPPO_RD_MASK = 1,
+  DPPO_RD_WEIGHT = 2,
+  DPPO_RD_MASK_WEIGHT = 3
+} dppo_rd_mode;
+
+/* Per-token scale s_t = scale * token_scale_t with
+ *  CONST:      scale = loss_scale
+ *  TOKEN_MEAN: scale = loss_scale / max(1, sum_t m_t)   (the E_t of Eq. 2 read as a mean
+ *              over loss-mask-valid tokens; band- and clip-removed tokens stay counted)  */
+typedef enum { DPPO_SCALE_CONST = 0, DPPO_SCALE_TOKEN_MEAN = 1 } dppo_scale_mode;
+
+/* Per-token flags (uint8), written when flags_out is non-NULL. */
+#define DPPO_FLAG_VALID 1u  /* m_t = 1: the row was evaluated                           */
+#define DPPO_FLAG_BAND 2u   /* band_lo <= r_d <= band_hi (Eq. 4)                         */
+#define DPPO_FLAG_PPO 4u    /* Eq. 3 active mask holds on r_s (not clipped)              */
+#define DPPO_FLAG_BAD_ID 8u /* valid row whose token id is outside [0, V)                */
+
+/* stats_out layout (int32[5]). rho_t = stats[3] / stats[0] is the Train-Infer Mask value
+ * that drives the PPO-EWMA automatic reset (Sec. 5.2).                                   */
+#define DPPO_STAT_N_VALID 0  /* sum_t m_t                                                 */
+#define DPPO_STAT_N_BAND 1   /* valid, good-id tokens inside the r_d band                  */
+#define DPPO_STAT_N_PPO 2    /* valid, good-id tokens with the PPO mask active             */
+#define DPPO_STAT_N_ACTIVE 3 /* PPO-active and (for MASK, MASK_WEIGHT) inside the band     */
+#define DPPO_STAT_N_BAD 4    /* valid rows with an out-of-range token id                   */
+#define DPPO_N_STATS 5
+
+/* Knobs of the decoupled MIS objective (Eq. 2, Eq. 3, Eq. 4; Table 1).
+ *  band_lo, band_hi:         r_d is kept iff band_lo <= r_d <= band_hi (inclusive, as in
+ *                            Eq. 4: M_[1/c, c] is band_lo = 1/c, band_hi = c; App. A's
+ *                            [1 - eps_1, 1 + eps_1] is the same with other bounds).
+ *                            0 <= band_lo <= band_hi; band_hi may be +inf.
+ *  clip_eps_lo, clip_eps_hi: PPO interval [1 - eps_lo, 1 + eps_hi] on r_s (Eq. 2; the
+ *                            asymmetric form of App. A). Both >= 0, finite.
+ *  rd_mode:                  a dppo_rd_mode.
+ *  scale_mode, loss_scale:   a dppo_scale_mode and a finite multiplier.            */
+typedef struct dppo_params {
+  float band_lo, band_hi;
+  float clip_eps_lo, clip_eps_hi;
+  int32_t rd_mode;
+  int32_t scale_mode;
+  float loss_scale;
+} dppo_params;
+
+/*
+ * logprob_fwd -- sampled-token log-probabilities log pi(y_t) = z[t, y_t] - lse_t with
+ * lse_t = log sum_v exp z[t, v] over the whole vocabulary (the token probabilities whose
+ * ratios Sec. 3.2 and Eq. 1 take). Also produces lp_ref from an old or proxy model's
+ * logits (Sec. 5.1 exact routes, Sec. 5.2 proxy).
+ *
+ *  logits     [T, ld] of `dtype` (DPPO_F32 or DPPO_BF16), row t at logits + t*ld; only
+ *             the first V entries of a row are read.
+ *  T >= 0, V >= 1, ld >= V; T < 2^31.
+ *  token_ids  [T] int64.
+ *  logp_out   [T] float32: log pi(y_t); NaN when y_t is outside [0, V).
+ *  lse_out    [T] float32 or NULL.
+ * Non-finite logits follow IEEE arithmetic: a row holding NaN or +inf, or only -inf, has
+ * lse = NaN. T = 0 enqueues nothing.
+ */
+dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
+                        const int64_t* token_ids, float* logp_out, float* lse_out,
+                        void* stream);
+
+/*
+ * decoupled_ppo_loss_fwd_bwd -- the fused loss stage: log-prob through a vocabulary-wide
+ * log-sum-exp, ratios r_s = pi_theta / pi_ref and r_d = pi_ref / mu_old (Eq. 1, Sec. 3.2),
+ * the band decision M(r_d) (Eq. 4), the sign-dependent PPO decision on r_s (Eq. 3), the
+ * per-token loss l_t = -wd_t * min(r_s A, clip(r_s, 1-eps_lo, 1+eps_hi) A) (Eq. 2), and,
+ * when dlogits is non-NULL, the gradient of L = sum_t m_t s_t l_t with respect to the
+ * logits in MIS form (Sec. 3.1):
+ *     dlogits[t, v] = w_t * (softmax(z_t)[v] - 1{v = y_t}),
+ *     w_t = m_t * s_t * wd_t * r_s * A_t  if PPO-active (and, for MASK modes, in band),
+ *     w_t = 0                              otherwise.
+ * r_d, the band and lp_ref are constants with respect to theta.
+ *
+ *  logits        [T, ld] of dtype; dlogits (if non-NULL) [T, ld_dlogits] of the same
+ *                dtype. dlogits may alias logits only exactly (same pointer and stride);
+ *                any other overlap is DPPO_ERR_INVALID_ARG.
+ *  token_ids     [T] int64.   logp_mu_old, logp_ref, advantages: [T] float32.
+ *  loss_mask     [T] uint8 or NULL (all 1). Rows with m_t = 0 are not read: lp 0, loss 0,
+ *                flags 0, and a zero dlogits row.
+ *  token_scale   [T] float32 or NULL (all 1).
+ *  p             host pointer to the parameters.
+ *  logp_out      [T] float32: lp_theta (0 on masked rows, NaN on bad ids).
+ *  loss_tok_out  [T] float32: l_t (before m_t and s_t).
+ *  loss_out      [1] float32: L = sum_t m_t s_t l_t, summed in a fixed order in float64
+ *                (bitwise reproducible run to run).
+ *  flags_out     [T] uint8 or NULL.
+ *  stats_out     [5] int32 (see DPPO_STAT_*); overwritten by the call.
+ * A valid row with y_t outside [0, V) gets lp NaN, l_t = 0, w_t = 0, a zero dlogits row,
+ * flags VALID|BAD_ID, and counts in stats[4] only. T = 0 writes loss 0 and zero stats.
+ */
+dppo_status decoupled_ppo_loss_fwd_bwd(
+    const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
+    const int64_t* token_ids, const float* logp_mu_old, const float* logp_ref,
+    const float* advantages, const uint8_t* loss_mask, const float* token_scale,
+    const dppo_params* p, float* logp_out, float* loss_tok_out, float* loss_out,
+    uint8_t* flags_out, void* dlogits, int64_t ld_dlogits, int32_t* stats_out, void* stream);
+
+/*
+ * ewma_proxy_update -- one step of the PPO-EWMA reference (Sec. 5.2, Eq. 5; App. B) on a
+ * flat buffer of n elements (proxy parameters, or per-token log-probs).
+ *  normalized = 1: w_t = 1 + beta * w_{t-1};
+ *                  x_prox <- x_new / w_t + beta * (w_{t-1} / w_t) * x_prox.
+ *                  With w_{t-1} = 0 (first step) x_prox <- x_new and x_prox is not read.
+ *  normalized = 0: fixed-decay form of Table 1: x_prox <- beta x_prox + (1 - beta) x_new;
+ *                  `w` is not used and may be NULL.
+ *  reset = 1:      automatic reset (Sec. 5.2): x_prox <- x_new, and *w = 1 when normalized.
+ *  x_prox, x_new   [n] device buffers of `dtype` (float32 math, bf16 stored with RNE);
+ *                  x_prox may not overlap x_new unless identical.
+ *  beta            in [0, 1).
+ *  w               host pointer: in w_{t-1} (0 before the first step), out w_t.
+ * n = 0 only updates *w.
+ */
+dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, int64_t n,
+                              float beta, double* w, int32_t reset, int32_t normalized,
+                              void* stream);
+
+/* Row-kernel policy, a testing and benchmarking hook: 0 = automatic (the
+ * register-resident kernel when the row fits, the two-pass streaming kernel otherwise),
+ * 1 = always the streaming kernel. Process-global; any other value is INVALID_ARG. */
+dppo_status dppo_set_path_policy(int32_t policy);
+
+/* Static description of a status code. */
+const char* dppo_strerror(dppo_status s);
+
+/* Message of the last failed call on this host thread ("" if none). */
+const char* dppo_last_error(void);
+
+/* ABI version of this header (incremented on incompatible changes). */
+#define DPPO_ABI_VERSION 1
+int32_t dppo_abi_version(void);
+
+/*
+ * Kernel timer for profiling. While enabled, the library records a pair of HIP events on
+ * the call's stream around every launch of the per-row loss-stage kernel (the one that
+ * streams the logits) and, on dppo_timer_read, synchronises those events and returns the
+ * summed elapsed time in milliseconds and the number of launches timed, then clears the
+ * record. Enabling allocates host-side event objects; it is process-global state, meant
+ * for one profiling thread.
+ */
+dppo_status dppo_timer_enable(int32_t on);
+dppo_status dppo_timer_read(double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPPO_H */

@@ -21,8 +21,8 @@ against the paper:
 * the MIS gradient form E[MIS * r * A * grad log pi] (Sec. 3.1), pushed through
   d log pi(y) / dz = onehot(y) - softmax(z);
 * the PPO-EWMA proxy recursion, its closed form, its centre of mass and the
-  staleness-aware decay (Sec. 4.2, Eq. 5; App. B);
-* the Train-Infer Mask value rho_t and the automatic reset rule (Sec. 4.2; App. E);
+  staleness-aware decay (Sec. 5.2, Eq. 5; App. B);
+* the Train-Infer Mask value rho_t and the automatic reset rule (Sec. 5.2; App. E);
 * the effective thresholds that interpolation proxies induce on the total ratio
   (Prop. 1; App. A; Table 4).
 
@@ -275,7 +275,7 @@ def stats_of(flags: np.ndarray, params: Params) -> np.ndarray:
     """[n_valid, n_band, n_ppo_active, n_active, n_bad_ids] from per-token flags.
 
     n_active counts tokens active after discrepancy masking and PPO clipping (the
-    numerator of the Train-Infer Mask value, Sec. 4.2); without a mask it counts PPO only.
+    numerator of the Train-Infer Mask value, Sec. 5.2); without a mask it counts PPO only.
     """
     f = flags.astype(np.int64)
     valid = (f & FLAG_VALID) != 0
@@ -324,7 +324,7 @@ def decoupled_ppo_loss(logits, ids, lp_mu, lp_ref, adv, mask=None, token_scale=N
 
 
 # ---------------------------------------------------------------------------------------
-# PPO-EWMA proxy (Sec. 4.2, Eq. 5; App. B) and its reset rule
+# PPO-EWMA proxy (Sec. 5.2, Eq. 5; App. B) and its reset rule
 # ---------------------------------------------------------------------------------------
 def ewma_normalized_step(x_prox, x_new, beta, w_prev):
     """One step of the normalised recursion of App. B.
@@ -346,7 +346,7 @@ def ewma_fixed_step(x_prox, x_new, beta):
 
 
 def ewma_reset():
-    """Automatic reset (Sec. 4.2): x_prox <- x_new, and the normaliser restarts at w = 1."""
+    """Automatic reset (Sec. 5.2): x_prox <- x_new, and the normaliser restarts at w = 1."""
     return 1.0
 
 
@@ -365,7 +365,7 @@ def ewma_center_of_mass(beta):
 
 
 def beta_from_window(w_stale):
-    """Staleness-aware decay beta = W / (W + 2) (Sec. 4.2; App. B)."""
+    """Staleness-aware decay beta = W / (W + 2) (Sec. 5.2; App. B)."""
     return w_stale / (w_stale + 2.0)
 
 
@@ -385,7 +385,7 @@ def ppo_clip_ratio(stats) -> float:
 
 
 def reset_schedule(rhos, tau=0.9, patience=1):
-    """Reset decisions for a sequence of rho_t values (Sec. 4.2; App. E).
+    """Reset decisions for a sequence of rho_t values (Sec. 5.2; App. E).
 
     A reset fires when rho_t < tau has held for `patience` consecutive steps; the streak
     then restarts from zero.

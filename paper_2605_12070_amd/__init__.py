@@ -1,0 +1,264 @@
+"""MI355X (gfx950) loss stage of decoupled off-policy PPO (arXiv 2605.12070).
+
+Thin Python binding over libdppo.so: every function here only checks tensors and passes
+device pointers and the current HIP stream to the C ABI (include/dppo.h); all arithmetic
+runs in the library's kernels. PyTorch supplies device memory and streams.
+
+    from paper_2605_12070_amd import decoupled_ppo_loss_fwd_bwd
+    res = decoupled_ppo_loss_fwd_bwd(logits, ids, lp_mu, lp_ref, adv)
+    res.loss, res.logp, res.dlogits, res.stats
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib
+from ._lib import (DppoError, FLAG_BAD_ID, FLAG_BAND, FLAG_PPO, FLAG_VALID,  # noqa: F401
+                   RD_MODES, SCALE_MODES, STAT_N_ACTIVE, STAT_N_BAD, STAT_N_BAND, STAT_N_PPO,
+                   STAT_N_VALID)
+
+__all__ = [
+    "logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "ewma_proxy_update", "LossResult",
+    "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
+    "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer",
+]
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return _lib.DPPO_BF16
+    if t.dtype == torch.float32:
+        return _lib.DPPO_F32
+    raise TypeError(f"logits must be bfloat16 or float32, got {t.dtype}")
+
+
+def _matrix(t: torch.Tensor, name: str):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D tensor with unit stride in its last dim")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    return t.data_ptr(), t.shape[0], t.shape[1], t.stride(0)
+
+
+def _vec(t, T, dtype, name, dev, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if t.dtype != dtype or t.dim() != 1 or t.shape[0] != T or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous [{T}] {dtype} tensor")
+    if t.device != dev:
+        raise ValueError(f"{name} must live on {dev}")
+    return t.data_ptr()
+
+
+def logprob_fwd(logits: torch.Tensor, token_ids: torch.Tensor, with_lse: bool = False):
+    """log pi(y_t) for every row of logits [T, V] (bf16 or fp32). Returns lp [T] fp32,
+    or (lp, lse) when with_lse."""
+    ptr, T, V, ld = _matrix(logits, "logits")
+    dev = logits.device
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    lp = torch.empty(T, dtype=torch.float32, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if with_lse else None
+    st = _lib.lib().logprob_fwd(ptr, _dtype_code(logits), T, V, ld, ids, lp.data_ptr(),
+                                lse.data_ptr() if lse is not None else None, _stream(dev))
+    _lib.check(st, "logprob_fwd")
+    return (lp, lse) if with_lse else lp
+
+
+@dataclass
+class LossResult:
+    loss: torch.Tensor          # [1] fp32: sum_t m_t s_t l_t
+    logp: torch.Tensor          # [T] fp32: log pi_theta(y_t)
+    loss_tok: torch.Tensor      # [T] fp32: l_t
+    flags: torch.Tensor | None  # [T] uint8
+    stats: torch.Tensor         # [5] int32
+    dlogits: torch.Tensor | None
+
+
+def decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advantages,
+                               loss_mask=None, token_scale=None, *, band=(0.5, 2.0),
+                               clip_eps=(0.2, 0.2), rd_mode="mask_weight",
+                               scale_mode="token_mean", loss_scale=1.0, want_dlogits=True,
+                               dlogits=None, want_flags=True, out: LossResult | None = None
+                               ) -> LossResult:
+    """Fused loss stage: log-prob, ratios, band and clip decisions, per-token loss, stats and
+    dlogits = w (softmax - onehot). `dlogits` may be the logits tensor itself (in place) or
+    a preallocated tensor; `out` reuses all output buffers."""
+    ptr, T, V, ld = _matrix(logits, "logits")
+    dev = logits.device
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    mu = _vec(logp_mu_old, T, torch.float32, "logp_mu_old", dev)
+    ref = _vec(logp_ref, T, torch.float32, "logp_ref", dev)
+    adv = _vec(advantages, T, torch.float32, "advantages", dev)
+    msk = _vec(loss_mask, T, torch.uint8, "loss_mask", dev, optional=True)
+    tsc = _vec(token_scale, T, torch.float32, "token_scale", dev, optional=True)
+    if rd_mode not in RD_MODES or scale_mode not in SCALE_MODES:
+        raise ValueError(f"rd_mode in {list(RD_MODES)}, scale_mode in {list(SCALE_MODES)}")
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=dev)
+        out = LossResult(
+            loss=torch.empty(1, **f32), logp=torch.empty(T, **f32),
+            loss_tok=torch.empty(T, **f32),
+            flags=torch.empty(T, dtype=torch.uint8, device=dev) if want_flags else None,
+            stats=torch.empty(_lib.N_STATS, dtype=torch.int32, device=dev), dlogits=None)
+    if want_dlogits:
+        if dlogits is None:
+            dlogits = out.dlogits if out.dlogits is not None else torch.empty_like(logits)
+        if dlogits.dtype != logits.dtype or dlogits.shape != logits.shape or dlogits.stride(1) != 1:
+            raise ValueError("dlogits must match logits in dtype and shape, unit last stride")
+        out.dlogits = dlogits
+        d_ptr, ldd = dlogits.data_ptr(), dlogits.stride(0)
+    else:
+        out.dlogits = None
+        d_ptr, ldd = None, 0
+    p = _lib.DppoParams(float(band[0]), float(band[1]), float(clip_eps[0]), float(clip_eps[1]),
+                        RD_MODES[rd_mode], SCALE_MODES[scale_mode], float(loss_scale))
+    st = _lib.lib().decoupled_ppo_loss_fwd_bwd(
+        ptr, _dtype_code(logits), T, V, ld, ids, mu, ref, adv, msk, tsc, C.byref(p),
+        out.logp.data_ptr(), out.loss_tok.data_ptr(), out.loss.data_ptr(),
+        out.flags.data_ptr() if out.flags is not None else None, d_ptr, ldd,
+        out.stats.data_ptr(), _stream(dev))
+    _lib.check(st, "decoupled_ppo_loss_fwd_bwd")
+    return out
+
+
+def ewma_proxy_update(x_prox: torch.Tensor, x_new: torch.Tensor, beta: float, w: float = 0.0,
+                      reset: bool = False, normalized: bool = True) -> float:
+    """One PPO-EWMA step on a flat buffer (in place on x_prox). Returns the new normaliser
+    w_t (normalized form) or w unchanged (fixed-decay form)."""
+    if x_prox.dtype != x_new.dtype or x_prox.numel() != x_new.numel():
+        raise ValueError("x_prox and x_new must have the same dtype and size")
+    if not (x_prox.is_contiguous() and x_new.is_contiguous() and x_prox.is_cuda and x_new.is_cuda):
+        raise ValueError("x_prox and x_new must be contiguous GPU tensors")
+    code = _dtype_code(x_prox)
+    wv = C.c_double(float(w))
+    st = _lib.lib().ewma_proxy_update(x_prox.data_ptr(), x_new.data_ptr(), code, x_prox.numel(),
+                                      float(beta), C.byref(wv), int(bool(reset)),
+                                      int(bool(normalized)), _stream(x_prox.device))
+    _lib.check(st, "ewma_proxy_update")
+    return wv.value
+
+
+def set_path_policy(policy: str):
+    """'auto' (register-resident rows when they fit) or 'stream' (always two-pass)."""
+    code = {"auto": 0, "stream": 1}[policy]
+    _lib.check(_lib.lib().dppo_set_path_policy(code), "dppo_set_path_policy")
+
+
+class KernelTimer:
+    """HIP-event timing of the per-row kernel launches made while the timer is on."""
+
+    def __enter__(self):
+        _lib.check(_lib.lib().dppo_timer_enable(1), "dppo_timer_enable")
+        return self
+
+    def read(self):
+        ms = C.c_double(0.0)
+        n = C.c_int64(0)
+        _lib.check(_lib.lib().dppo_timer_read(C.byref(ms), C.byref(n)), "dppo_timer_read")
+        return ms.value, n.value
+
+    def __exit__(self, *exc):
+        _lib.lib().dppo_timer_enable(0)
+
+
+# ------------------------------------------------------------------ host-side controller
+def beta_from_window(w_stale: float) -> float:
+    """Staleness-aware decay beta = W / (W + 2): the EWMA centre of mass beta / (1 - beta)
+    sits at the middle of a version window of width W (Sec. 5.2; App. B)."""
+    if w_stale < 0:
+        raise ValueError("staleness window must be >= 0")
+    return w_stale / (w_stale + 2.0)
+
+
+def train_infer_mask_value(stats) -> float:
+    """rho_t = n_active / n_valid (1 when no token is valid)."""
+    n_valid = int(stats[STAT_N_VALID])
+    return 1.0 if n_valid == 0 else int(stats[STAT_N_ACTIVE]) / n_valid
+
+
+def ppo_clip_ratio(stats) -> float:
+    """Fraction of valid tokens removed by PPO clipping."""
+    n_valid = int(stats[STAT_N_VALID])
+    return 0.0 if n_valid == 0 else 1.0 - int(stats[STAT_N_PPO]) / n_valid
+
+
+class EwmaProxy:
+    """PPO-EWMA reference with automatic reset (Sec. 5.2; App. B; App. E).
+
+    Holds the proxy buffer (parameters or per-token log-probs), the normaliser w and the
+    low-rho streak. `step(x_new, stats)` reads the loss stage's stats (one small
+    device-to-host copy), resets when rho_t < tau has held for `patience` consecutive
+    steps, and otherwise applies the normalised recursion. Its state (buffer, w, streak)
+    is what a checkpoint must save.
+    """
+
+    def __init__(self, x0: torch.Tensor, beta: float, tau: float = 0.9, patience: int = 1,
+                 normalized: bool = True):
+        if not 0.0 <= beta < 1.0:
+            raise ValueError("beta must lie in [0, 1)")
+        self.x = x0.clone()
+        self.beta = float(beta)
+        self.tau = float(tau)
+        self.patience = int(patience)
+        self.normalized = normalized
+        self.w = 1.0          # x0 is theta^(0): one step of history
+        self.streak = 0
+        self.resets = 0
+        self.last_rho = 1.0
+
+    def decide_reset(self, stats) -> bool:
+        rho = train_infer_mask_value(stats)
+        self.last_rho = rho
+        self.streak = self.streak + 1 if rho < self.tau else 0
+        fire = self.streak >= self.patience
+        if fire:
+            self.streak = 0
+        return fire
+
+    def step(self, x_new: torch.Tensor, stats=None) -> bool:
+        if stats is not None and not isinstance(stats, (list, tuple)):
+            stats = stats.tolist()
+        reset = self.decide_reset(stats) if stats is not None else False
+        self.w = ewma_proxy_update(self.x, x_new, self.beta, self.w, reset=reset,
+                                   normalized=self.normalized)
+        if reset:
+            self.resets += 1
+        return reset
+
+    def state_dict(self):
+        return dict(x=self.x, w=self.w, streak=self.streak, resets=self.resets,
+                    beta=self.beta, tau=self.tau, patience=self.patience,
+                    normalized=self.normalized)
+
+    def load_state_dict(self, sd):
+        self.x.copy_(sd["x"])
+        for k in ("w", "streak", "resets", "beta", "tau", "patience", "normalized"):
+            setattr(self, k, sd[k])
+
+
+class DecoupledPPOLoss(torch.autograd.Function):
+    """Autograd wrapper: forward runs the fused kernel (loss and dlogits at once); backward
+    returns grad_output * dlogits (one extra elementwise pass when grad_output != 1)."""
+
+    @staticmethod
+    def forward(ctx, logits, token_ids, logp_mu_old, logp_ref, advantages, loss_mask,
+                token_scale, kwargs):
+        res = decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advantages,
+                                         loss_mask, token_scale, **(kwargs or {}))
+        ctx.save_for_backward(res.dlogits)
+        ctx.mark_non_differentiable(res.logp, res.stats)
+        return res.loss[0], res.logp, res.stats
+
+    @staticmethod
+    def backward(ctx, g_loss, g_lp, g_stats):
+        (d,) = ctx.saved_tensors
+        return (d * g_loss.to(d.dtype), None, None, None, None, None, None, None)

@@ -1,0 +1,291 @@
+// C-ABI layer: argument checks (all on the host, before any HIP call), kernel selection,
+// launches on the caller's stream, error reporting and the profiling timer.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "dppo.h"
+#include "ewma.h"
+#include "loss_stage.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+int g_path_policy = dppo::kForceAuto;
+
+dppo_status fail(dppo_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+dppo_status fail(dppo_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+dppo_status hip_fail(hipError_t e, const char* what) {
+  return fail(DPPO_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int esize_of(int32_t dtype) { return dtype == DPPO_BF16 ? 2 : 4; }
+
+// [begin, end) byte range of a [T, ld] matrix whose rows hold V used elements.
+std::pair<uintptr_t, uintptr_t> span_of(const void* base, int64_t T, int64_t V, int64_t ld, int es) {
+  const uintptr_t b = (uintptr_t)base;
+  return {b, b + (uintptr_t)(((T - 1) * ld + V) * es)};
+}
+
+bool overlaps(std::pair<uintptr_t, uintptr_t> a, std::pair<uintptr_t, uintptr_t> b) {
+  return a.first < b.second && b.first < a.second;
+}
+
+// ------------------------------------------------------------------ kernel timer
+struct KernelTimer {
+  std::mutex mu;
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pool;
+  size_t used = 0;
+};
+KernelTimer g_timer;
+
+// Returns the event pair to record around the next launch, or nullptr when disabled.
+std::pair<hipEvent_t, hipEvent_t>* timer_slot() {
+  std::lock_guard<std::mutex> lk(g_timer.mu);
+  if (!g_timer.on) return nullptr;
+  if (g_timer.used == g_timer.pool.size()) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return nullptr;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return nullptr;
+    }
+    g_timer.pool.emplace_back(a, b);
+  }
+  return &g_timer.pool[g_timer.used++];
+}
+
+dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgs& args, int64_t T,
+                        hipStream_t st) {
+  auto* ev = timer_slot();
+  if (ev) (void)hipEventRecord(ev->first, st);
+  void* kargs[] = {(void*)&args};
+  hipError_t e = hipLaunchKernel((const void*)L.fn, dim3((unsigned)T), dim3((unsigned)L.threads),
+                                 kargs, 0, st);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (ev) (void)hipEventRecord(ev->second, st);
+  if (e != hipSuccess) return hip_fail(e, "row kernel launch");
+  return DPPO_OK;
+}
+
+dppo_status check_matrix(const void* p, int32_t dtype, int64_t T, int64_t V, int64_t ld,
+                         const char* name) {
+  if (dtype != DPPO_F32 && dtype != DPPO_BF16)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (T < 0 || T > 0x7FFFFFFF) return fail(DPPO_ERR_INVALID_ARG, "T = %lld out of [0, 2^31)", (long long)T);
+  if (V < 1 || V > 0x7FFFFFFF) return fail(DPPO_ERR_INVALID_ARG, "V = %lld out of [1, 2^31)", (long long)V);
+  if (ld < V) return fail(DPPO_ERR_INVALID_ARG, "%s stride %lld < V = %lld", name, (long long)ld, (long long)V);
+  if (T > 0 && p == nullptr) return fail(DPPO_ERR_INVALID_ARG, "%s is NULL", name);
+  return DPPO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dppo_strerror(dppo_status s) {
+  switch (s) {
+    case DPPO_OK: return "success";
+    case DPPO_ERR_INVALID_ARG: return "invalid argument";
+    case DPPO_ERR_UNSUPPORTED: return "unsupported request";
+    case DPPO_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* dppo_last_error(void) { return g_last_error.c_str(); }
+
+int32_t dppo_abi_version(void) { return DPPO_ABI_VERSION; }
+
+dppo_status dppo_set_path_policy(int32_t policy) {
+  if (policy != dppo::kForceAuto && policy != dppo::kForceStream)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown path policy %d", (int)policy);
+  g_path_policy = policy;
+  return DPPO_OK;
+}
+
+dppo_status dppo_timer_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_timer.mu);
+  if (!on) {
+    for (auto& pr : g_timer.pool) {
+      (void)hipEventDestroy(pr.first);
+      (void)hipEventDestroy(pr.second);
+    }
+    g_timer.pool.clear();
+  }
+  g_timer.used = 0;
+  g_timer.on = on != 0;
+  return DPPO_OK;
+}
+
+dppo_status dppo_timer_read(double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches) return fail(DPPO_ERR_INVALID_ARG, "dppo_timer_read: NULL output");
+  std::lock_guard<std::mutex> lk(g_timer.mu);
+  double acc = 0.0;
+  for (size_t i = 0; i < g_timer.used; ++i) {
+    hipError_t e = hipEventSynchronize(g_timer.pool[i].second);
+    if (e != hipSuccess) return hip_fail(e, "timer event sync");
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, g_timer.pool[i].first, g_timer.pool[i].second);
+    if (e != hipSuccess) return hip_fail(e, "timer elapsed");
+    acc += ms;
+  }
+  *total_ms = acc;
+  *launches = (int64_t)g_timer.used;
+  g_timer.used = 0;
+  return DPPO_OK;
+}
+
+dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
+                        const int64_t* token_ids, float* logp_out, float* lse_out, void* stream) {
+  dppo_status s = check_matrix(logits, dtype, T, V, ld, "logits");
+  if (s != DPPO_OK) return s;
+  if (T > 0 && (!token_ids || !logp_out))
+    return fail(DPPO_ERR_INVALID_ARG, "logprob_fwd: token_ids and logp_out are required");
+  if (T == 0) return DPPO_OK;
+  const int es = esize_of(dtype);
+  const bool aligned = aligned16(logits) && ((ld * es) % 16 == 0);
+  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
+  dppo::RowArgs a{};
+  a.logits = logits;
+  a.ld = ld;
+  a.ids = token_ids;
+  a.lp_out = logp_out;
+  a.lse_out = lse_out;
+  a.V = (int32_t)V;
+  a.mode = dppo::kModeLogprob;
+  return launch_rows(L, a, T, (hipStream_t)stream);
+}
+
+dppo_status decoupled_ppo_loss_fwd_bwd(
+    const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
+    const int64_t* token_ids, const float* logp_mu_old, const float* logp_ref,
+    const float* advantages, const uint8_t* loss_mask, const float* token_scale,
+    const dppo_params* p, float* logp_out, float* loss_tok_out, float* loss_out,
+    uint8_t* flags_out, void* dlogits, int64_t ld_dlogits, int32_t* stats_out, void* stream) {
+  dppo_status s = check_matrix(logits, dtype, T, V, ld, "logits");
+  if (s != DPPO_OK) return s;
+  if (!p) return fail(DPPO_ERR_INVALID_ARG, "params pointer is NULL");
+  if (!loss_out || !stats_out) return fail(DPPO_ERR_INVALID_ARG, "loss_out and stats_out are required");
+  if (T > 0 && (!token_ids || !logp_mu_old || !logp_ref || !advantages || !logp_out || !loss_tok_out))
+    return fail(DPPO_ERR_INVALID_ARG,
+                "token_ids, logp_mu_old, logp_ref, advantages, logp_out, loss_tok_out are required");
+  if (std::isnan(p->band_lo) || std::isnan(p->band_hi) || p->band_lo < 0.0f || p->band_lo > p->band_hi)
+    return fail(DPPO_ERR_INVALID_ARG, "band [%g, %g] must satisfy 0 <= lo <= hi", p->band_lo, p->band_hi);
+  if (!(p->clip_eps_lo >= 0.0f) || !(p->clip_eps_hi >= 0.0f) || !std::isfinite(p->clip_eps_lo) ||
+      !std::isfinite(p->clip_eps_hi))
+    return fail(DPPO_ERR_INVALID_ARG, "clip eps (%g, %g) must be finite and >= 0", p->clip_eps_lo, p->clip_eps_hi);
+  if (!std::isfinite(p->loss_scale)) return fail(DPPO_ERR_INVALID_ARG, "loss_scale must be finite");
+  if (p->rd_mode < DPPO_RD_NONE || p->rd_mode > DPPO_RD_MASK_WEIGHT)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown rd_mode %d", (int)p->rd_mode);
+  if (p->scale_mode != DPPO_SCALE_CONST && p->scale_mode != DPPO_SCALE_TOKEN_MEAN)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown scale_mode %d", (int)p->scale_mode);
+  const int es = esize_of(dtype);
+  if (dlogits && T > 0) {
+    if (ld_dlogits < V)
+      return fail(DPPO_ERR_INVALID_ARG, "dlogits stride %lld < V = %lld", (long long)ld_dlogits, (long long)V);
+    const bool same = dlogits == logits && ld_dlogits == ld;
+    if (!same && overlaps(span_of(logits, T, V, ld, es), span_of(dlogits, T, V, ld_dlogits, es)))
+      return fail(DPPO_ERR_INVALID_ARG, "dlogits overlaps logits without aliasing them exactly");
+  }
+  hipStream_t st = (hipStream_t)stream;
+  dppo::launch_prep_stats(loss_mask, T, stats_out, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "prep_stats launch");
+  if (T > 0) {
+    const bool aligned = aligned16(logits) && ((ld * es) % 16 == 0) &&
+                         (!dlogits || (aligned16(dlogits) && (ld_dlogits * es) % 16 == 0));
+    const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, dlogits != nullptr, g_path_policy);
+    dppo::RowArgs a{};
+    a.logits = logits;
+    a.ld = ld;
+    a.dlogits = dlogits;
+    a.ldd = ld_dlogits;
+    a.ids = token_ids;
+    a.lp_mu = logp_mu_old;
+    a.lp_ref = logp_ref;
+    a.adv = advantages;
+    a.mask = loss_mask;
+    a.tscale = token_scale;
+    a.lp_out = logp_out;
+    a.loss_tok = loss_tok_out;
+    a.flags = flags_out;
+    a.stats = stats_out;
+    a.V = (int32_t)V;
+    a.mode = dppo::kModeLoss;
+    a.band_lo = p->band_lo;
+    a.band_hi = p->band_hi;
+    a.clip_lo = 1.0f - p->clip_eps_lo;
+    a.clip_hi = 1.0f + p->clip_eps_hi;
+    a.loss_scale = p->loss_scale;
+    a.rd_mode = p->rd_mode;
+    a.scale_mode = p->scale_mode;
+    s = launch_rows(L, a, T, st);
+    if (s != DPPO_OK) return s;
+  }
+  dppo::launch_loss_sum(loss_tok_out, loss_mask, token_scale, stats_out, T, p->loss_scale,
+                        p->scale_mode, loss_out, st);
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "loss_sum launch");
+  return DPPO_OK;
+}
+
+dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, int64_t n,
+                              float beta, double* w, int32_t reset, int32_t normalized,
+                              void* stream) {
+  if (dtype != DPPO_F32 && dtype != DPPO_BF16)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (n < 0) return fail(DPPO_ERR_INVALID_ARG, "n = %lld < 0", (long long)n);
+  if (!(beta >= 0.0f && beta < 1.0f)) return fail(DPPO_ERR_INVALID_ARG, "beta = %g not in [0, 1)", beta);
+  if (n > 0 && (!x_prox || !x_new)) return fail(DPPO_ERR_INVALID_ARG, "x_prox and x_new are required");
+  if (normalized && !w) return fail(DPPO_ERR_INVALID_ARG, "w is required in normalized mode");
+  if (normalized && !(std::isfinite(*w) && *w >= 0.0))
+    return fail(DPPO_ERR_INVALID_ARG, "w_{t-1} = %g must be finite and >= 0", normalized ? *w : 0.0);
+  const int es = esize_of(dtype);
+  if (n > 0 && x_prox != x_new &&
+      overlaps(span_of(x_prox, 1, n, n, es), span_of(x_new, 1, n, n, es)))
+    return fail(DPPO_ERR_INVALID_ARG, "x_prox overlaps x_new without aliasing them exactly");
+
+  // Coefficients of x_prox <- ca * x_new + cb * x_prox, in double on the host.
+  double ca, cb, w_new = normalized ? *w : 0.0;
+  if (reset) {
+    ca = 1.0;
+    cb = 0.0;
+    if (normalized) w_new = 1.0;
+  } else if (normalized) {
+    const double wp = *w;
+    w_new = 1.0 + (double)beta * wp;
+    ca = 1.0 / w_new;
+    cb = (double)beta * wp / w_new;
+  } else {
+    ca = 1.0 - (double)beta;
+    cb = (double)beta;
+  }
+  if (n > 0) {
+    const bool aligned = aligned16(x_prox) && aligned16(x_new);
+    const hipError_t e = dppo::launch_ewma(x_prox, x_new, dtype == DPPO_BF16, n, (float)ca,
+                                           (float)cb, cb != 0.0, aligned, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "ewma launch");
+  }
+  if (normalized) *w = w_new;
+  return DPPO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,138 @@
+// Device-side helpers for the gfx950 loss-stage kernels.
+//
+// Numerics of the vocabulary-wide log-sum-exp. Every thread keeps its share of a row's
+// logits and works in log2 units: with n = L * m (L = log2 e, m = the thread's maximum,
+// rounded once to float), each element contributes e = 2^(z L - n), evaluated as one FMA
+// (z L is exact inside the FMA, one rounding) and one v_exp_f32. Thread partials (n, s)
+// merge as N = max n, S = sum s * 2^(n - N), where n - N is a difference of floats (exact
+// when the shifts are close), so lse2 = N + log2 S carries about one ulp of error however
+// large the logits are. lse = lse2 * ln 2 and softmax(z)[v] = 2^(z L - lse2).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dppo {
+
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr uint32_t kBf16NegInfPair = 0xFF80FF80u;  // two bf16 -inf
+constexpr uint32_t kF32NegInf = 0xFF800000u;
+
+// 2^x on the transcendental unit (v_exp_f32); about 1 ulp for normal results.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// max(a, b, c) in one v_max3_f32. A quiet-NaN operand is ignored, as by fmaxf; NaN logits
+// still reach the sum of exponentials, which turns NaN.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// bf16 halves of a 32-bit word as exact floats.
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+}
+__device__ __forceinline__ uint16_t to_bf16(float x) {
+  return (uint16_t)(pack_bf16(x, 0.0f) & 0xFFFFu);
+}
+
+// Two floats -> two fp16, round to nearest even (v_cvt_pk_f16_f32).
+__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
+  f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2));
+}
+
+// fp16 half of a word times a float scale, fused (v_fma_mix_f32).
+__device__ __forceinline__ float f16_lo_mul(uint32_t u, float f) {
+  f16x2 h = __builtin_bit_cast(f16x2, u);
+  return __builtin_fmaf((float)h[0], f, 0.0f);
+}
+__device__ __forceinline__ float f16_hi_mul(uint32_t u, float f) {
+  f16x2 h = __builtin_bit_cast(f16x2, u);
+  return __builtin_fmaf((float)h[1], f, 0.0f);
+}
+
+// Merge two log2-domain partials (n, s) into (n, s). A partial with n = -inf is empty.
+__device__ __forceinline__ void merge_ns(float& n, float& s, float n2, float s2) {
+  const float N = fmaxf(n, n2);
+  const float fa = (n == N) ? 1.0f : exp2f(n - N);
+  const float fb = (n2 == N) ? 1.0f : exp2f(n2 - N);
+  s = s * fa + s2 * fb;
+  n = N;
+}
+
+// Workgroup-wide merge of (n, s); every thread returns the row result. `lds` holds
+// 2 * (NT / 64) + 2 floats. Fixed reduction order: the result is reproducible.
+template <int NT>
+__device__ __forceinline__ void block_merge_ns(float& n, float& s, float* lds) {
+  constexpr int NW = NT / 64;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float n2 = __shfl_xor(n, off, 64);
+    const float s2 = __shfl_xor(s, off, 64);
+    merge_ns(n, s, n2, s2);
+  }
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  if (NW > 1) {
+    if (lane == 0) {
+      lds[wave] = n;
+      lds[NW + wave] = s;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      n = lane < NW ? lds[lane] : -INFINITY;
+      s = lane < NW ? lds[NW + lane] : 0.0f;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const float n2 = __shfl_xor(n, off, 64);
+        const float s2 = __shfl_xor(s, off, 64);
+        merge_ns(n, s, n2, s2);
+      }
+      if (lane == 0) {
+        lds[2 * NW] = n;
+        lds[2 * NW + 1] = s;
+      }
+    }
+    __syncthreads();
+    n = lds[2 * NW];
+    s = lds[2 * NW + 1];
+  }
+}
+
+// Raw buffer resources (gfx9-family descriptor: stride 0, 32-bit data format). Loads past
+// num_records return zeros and stores past it are dropped, so a row's resource bounds
+// every access to that row.
+constexpr int kRsrcFlags = 0x00020000;
+constexpr int kAuxNT = 2;  // non-temporal cache policy bit for buffer accesses on gfx950
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, kRsrcFlags);
+}
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+__device__ __forceinline__ void buf_store16_nt(u32x4 v, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
+}
+
+// numpy-style minimum: NaN if either operand is NaN.
+__device__ __forceinline__ float nan_min(float a, float b) {
+  return (a != a || b != b) ? __builtin_nanf("") : fminf(a, b);
+}
+
+}  // namespace dppo

@@ -1,0 +1,102 @@
+// PPO-EWMA proxy update on a flat buffer (Sec. 5.2, Eq. 5; App. B of arXiv 2605.12070):
+// x_prox <- a * x_new + b * x_prox with host-computed coefficients (a, b). b = 0 means the
+// old contents are not read (first step, reset). HBM-bound: 16-byte loads and stores,
+// grid-stride loop, float32 arithmetic, bf16 storage rounded to nearest even.
+#include "dppo.h"
+#include "dppo_device.h"
+#include "ewma.h"
+
+namespace dppo {
+
+template <bool BF16, bool READ_OLD>
+__global__ __launch_bounds__(256) void ewma_kernel(void* xp_, const void* xn_,
+                                                   int64_t n, float ca, float cb) {
+  constexpr int E = BF16 ? 8 : 4;  // elements per 16-byte vector
+  const int64_t nvec = n / E;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  u32x4* xp = (u32x4*)xp_;
+  const u32x4* xn = (const u32x4*)xn_;
+  for (int64_t i = tid; i < nvec; i += stride) {
+    const u32x4 vn = __builtin_nontemporal_load(xn + i);
+    u32x4 vo = {0u, 0u, 0u, 0u};
+    if (READ_OLD) vo = xp[i];
+    u32x4 out;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (BF16) {
+        const float lo = READ_OLD ? __builtin_fmaf(cb, bf16_lo(vo[k]), ca * bf16_lo(vn[k])) : ca * bf16_lo(vn[k]);
+        const float hi = READ_OLD ? __builtin_fmaf(cb, bf16_hi(vo[k]), ca * bf16_hi(vn[k])) : ca * bf16_hi(vn[k]);
+        out[k] = pack_bf16(lo, hi);
+      } else {
+        const float x = __uint_as_float(vn[k]);
+        const float r = READ_OLD ? __builtin_fmaf(cb, __uint_as_float(vo[k]), ca * x) : ca * x;
+        out[k] = __float_as_uint(r);
+      }
+    }
+    xp[i] = out;
+  }
+  // tail elements (n not a multiple of the vector width)
+  const int64_t tail0 = nvec * E;
+  for (int64_t e = tail0 + tid; e < n; e += stride) {
+    if (BF16) {
+      uint16_t* p = (uint16_t*)xp_;
+      const float xnew = bf16_to_f32(((const uint16_t*)xn_)[e]);
+      const float r = READ_OLD ? __builtin_fmaf(cb, bf16_to_f32(p[e]), ca * xnew) : ca * xnew;
+      p[e] = to_bf16(r);
+    } else {
+      float* p = (float*)xp_;
+      const float xnew = ((const float*)xn_)[e];
+      p[e] = READ_OLD ? __builtin_fmaf(cb, p[e], ca * xnew) : ca * xnew;
+    }
+  }
+}
+
+// Unaligned buffers: element-wise.
+template <bool BF16, bool READ_OLD>
+__global__ __launch_bounds__(256) void ewma_kernel_scalar(void* xp_, const void* xn_, int64_t n,
+                                                          float ca, float cb) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
+    if (BF16) {
+      uint16_t* p = (uint16_t*)xp_;
+      const float xnew = bf16_to_f32(((const uint16_t*)xn_)[e]);
+      const float r = READ_OLD ? __builtin_fmaf(cb, bf16_to_f32(p[e]), ca * xnew) : ca * xnew;
+      p[e] = to_bf16(r);
+    } else {
+      float* p = (float*)xp_;
+      const float xnew = ((const float*)xn_)[e];
+      p[e] = READ_OLD ? __builtin_fmaf(cb, p[e], ca * xnew) : ca * xnew;
+    }
+  }
+}
+
+hipError_t launch_ewma(void* xp, const void* xn, bool bf16, int64_t n, float ca, float cb,
+                       bool read_old, bool aligned, hipStream_t st) {
+  const int64_t per_thread = aligned ? (bf16 ? 8 : 4) : 1;
+  int64_t blocks = (n / per_thread + 255) / 256;
+  // 256 CUs x 8 workgroups keeps every CU busy; the grid-stride loop covers the rest.
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  const dim3 g((unsigned)blocks), b(256);
+  if (aligned) {
+    if (bf16) {
+      if (read_old) ewma_kernel<true, true><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+      else ewma_kernel<true, false><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+    } else {
+      if (read_old) ewma_kernel<false, true><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+      else ewma_kernel<false, false><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+    }
+  } else {
+    if (bf16) {
+      if (read_old) ewma_kernel_scalar<true, true><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+      else ewma_kernel_scalar<true, false><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+    } else {
+      if (read_old) ewma_kernel_scalar<false, true><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+      else ewma_kernel_scalar<false, false><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace dppo

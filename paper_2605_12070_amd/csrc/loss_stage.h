@@ -1,0 +1,55 @@
+// Internal interface between the C-ABI layer and the loss-stage kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dppo {
+
+constexpr int kModeLogprob = 0;  // log-prob (and lse) only
+constexpr int kModeLoss = 1;     // decoupled PPO loss, optional dlogits
+
+constexpr int kForceAuto = 0;
+constexpr int kForceStream = 1;  // use the two-pass streaming kernel even when resident fits
+
+// Arguments of every per-row kernel (passed by value).
+struct RowArgs {
+  const void* logits;
+  int64_t ld;
+  void* dlogits;        // NULL: forward only
+  int64_t ldd;
+  const int64_t* ids;
+  const float* lp_mu;
+  const float* lp_ref;
+  const float* adv;
+  const uint8_t* mask;  // NULL: all valid
+  const float* tscale;  // NULL: all 1
+  float* lp_out;
+  float* loss_tok;
+  uint8_t* flags;       // NULL: not written
+  int32_t* stats;
+  float* lse_out;       // log-prob mode only, may be NULL
+  int32_t V;
+  int32_t mode;
+  float band_lo, band_hi;
+  float clip_lo, clip_hi;  // 1 - eps_lo, 1 + eps_hi
+  float loss_scale;
+  int32_t rd_mode;
+  int32_t scale_mode;
+};
+
+typedef void (*RowKernel)(RowArgs);
+
+struct RowLaunch {
+  RowKernel fn = nullptr;
+  int threads = 0;
+  bool resident = false;
+};
+
+RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force);
+void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream_t st);
+void launch_loss_sum(const float* loss_tok, const uint8_t* mask, const float* tscale,
+                     const int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
+                     float* loss_out, hipStream_t st);
+
+}  // namespace dppo

@@ -1,0 +1,693 @@
+// Per-row kernels of the loss stage (gfx950): vocabulary-wide log-sum-exp, the decoupled
+// MIS token math (Eq. 1-4 of arXiv 2605.12070) and the fused dlogits sweep, plus the two
+// small kernels around them (valid-token count, deterministic loss sum).
+//
+// Launch shape: one workgroup per token row. A row of V = 151936 bf16 logits (297 KiB) is
+// loaded once with 16-byte loads and kept in registers (1024 threads x 19 x 16 B); the
+// thread's exponentials replace the logits in the same registers as fp16 pairs, so the
+// backward sweep reads nothing from memory and writes dlogits once with 16-byte
+// non-temporal stores. Rows longer than the register budget, or unaligned rows, use a
+// streaming kernel that reads the row twice.
+#include "dppo.h"
+#include "dppo_device.h"
+#include "loss_stage.h"
+
+namespace dppo {
+
+// ---------------------------------------------------------------------------------------
+// Token math shared by every row kernel (runs on one thread per row).
+// ---------------------------------------------------------------------------------------
+struct TokenOut {
+  float lp;      // log pi_theta(y)
+  float loss;    // l_t = -wd * min(r_s A, clip(r_s) A)
+  float w;       // MIS weight: d L / d lp_theta = -w, dlogits = w (softmax - onehot)
+  float dy;      // dlogits at v = y: w (p_y - 1) = w expm1(lp)
+  uint8_t flags;
+};
+
+__device__ __forceinline__ TokenOut token_math(const RowArgs& a, int64_t row, float zy,
+                                               float lse2, float scale) {
+  TokenOut o;
+  const float lse = lse2 * kLn2;
+  const float lp = zy - lse;
+  o.lp = lp;
+  const float lp_ref = a.lp_ref[row];
+  const float lp_mu = a.lp_mu[row];
+  const float A = a.adv[row];
+  const float ts = a.tscale ? a.tscale[row] : 1.0f;
+  // Eq. 1 / Sec. 3.2: r_s = pi_theta / pi_ref, r_d = pi_ref / mu_old.
+  const float r_s = expf(lp - lp_ref);
+  const float r_d = expf(lp_ref - lp_mu);
+  // Eq. 4 band (inclusive) and Eq. 3 sign-dependent PPO mask (inclusive).
+  const bool band = (a.band_lo <= r_d) && (r_d <= a.band_hi);
+  const bool ppo = ((A >= 0.0f) && (r_s <= a.clip_hi)) || ((A < 0.0f) && (r_s >= a.clip_lo));
+  float wd;
+  bool gate;
+  switch (a.rd_mode) {
+    case DPPO_RD_NONE: wd = 1.0f; gate = ppo; break;
+    case DPPO_RD_MASK: wd = band ? 1.0f : 0.0f; gate = ppo && band; break;
+    case DPPO_RD_WEIGHT: wd = r_d; gate = ppo; break;
+    default: wd = band ? r_d : 0.0f; gate = ppo && band; break;
+  }
+  // Eq. 2 summand with numpy min semantics (NaN in, NaN out).
+  const float clipped = fminf(fmaxf(r_s, a.clip_lo), a.clip_hi);
+  const float sur = nan_min(r_s * A, clipped * A);
+  o.loss = -wd * sur;
+  const float s = scale * ts;
+  o.w = gate ? s * wd * r_s * A : 0.0f;
+  o.dy = o.w * expm1f(lp);
+  o.flags = (uint8_t)(DPPO_FLAG_VALID | (band ? DPPO_FLAG_BAND : 0u) | (ppo ? DPPO_FLAG_PPO : 0u));
+  return o;
+}
+
+__device__ __forceinline__ float row_scale(const RowArgs& a) {
+  if (a.scale_mode == DPPO_SCALE_TOKEN_MEAN) {
+    const int n = a.stats[DPPO_STAT_N_VALID];
+    return a.loss_scale / (float)(n > 1 ? n : 1);
+  }
+  return a.loss_scale;
+}
+
+__device__ __forceinline__ void count_stats(const RowArgs& a, uint8_t flags) {
+  const bool band = flags & DPPO_FLAG_BAND;
+  const bool ppo = flags & DPPO_FLAG_PPO;
+  const bool uses_mask = a.rd_mode == DPPO_RD_MASK || a.rd_mode == DPPO_RD_MASK_WEIGHT;
+  if (band) atomicAdd(&a.stats[DPPO_STAT_N_BAND], 1);
+  if (ppo) atomicAdd(&a.stats[DPPO_STAT_N_PPO], 1);
+  if (ppo && (band || !uses_mask)) atomicAdd(&a.stats[DPPO_STAT_N_ACTIVE], 1);
+}
+
+// Rows that are not evaluated (loss mask 0, or a bad token id on a valid row).
+template <typename Tin, int NT>
+__device__ void skip_row(const RowArgs& a, int64_t row, bool valid) {
+  if (a.dlogits) {
+    Tin* d = (Tin*)a.dlogits + row * a.ldd;
+    for (int v = threadIdx.x; v < a.V; v += NT) d[v] = (Tin)0;
+  }
+  if (threadIdx.x == 0) {
+    a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
+    a.loss_tok[row] = 0.0f;
+    if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
+    if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+  }
+}
+
+// Zero dlogits row for the register-resident paths: NC 16-byte buffer stores per thread
+// (stores past the row are dropped by the buffer range check) plus a ragged tail.
+template <int NT, int NC, int ES>
+__device__ void skip_row_resident(const RowArgs& a, int64_t row, bool valid) {
+  if (a.dlogits) {
+    constexpr int E = 16 / ES;
+    char* d = (char*)a.dlogits + row * a.ldd * ES;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(d, a.V * ES);
+    const int nfull = a.V / E;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      if (c * NT + (int)threadIdx.x < nfull) buf_store16_nt(z, rd, threadIdx.x * 16, c * NT * 16);
+    for (int e = nfull * E + threadIdx.x; e < a.V; e += NT) {
+      if (ES == 2) ((uint16_t*)d)[e] = 0;
+      else ((float*)d)[e] = 0.0f;
+    }
+  }
+  if (threadIdx.x == 0) {
+    a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
+    a.loss_tok[row] = 0.0f;
+    if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
+    if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+  }
+}
+
+// Per-thread factor turning stored exponentials 2^(zL - n_mine) into w * softmax.
+__device__ __forceinline__ float row_factor(float w, float n_mine, float lse2) {
+  if (lse2 != lse2) return __builtin_nanf("");
+  return (n_mine == -INFINITY) ? 0.0f : w * exp2f(n_mine - lse2);
+}
+
+// Thread 0 finishes a row: writes per-token outputs, counts stats, and publishes the
+// backward constants (w, lse2, dy) in LDS. Returns through `bc`.
+struct Bcast {
+  float w, lse2, dy;
+};
+
+__device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float zy,
+                                           float lse2, bool good, Bcast* bc) {
+  if (a.mode == kModeLogprob) {
+    if (threadIdx.x == 0) {
+      a.lp_out[row] = good ? zy - lse2 * kLn2 : __builtin_nanf("");
+      if (a.lse_out) a.lse_out[row] = lse2 * kLn2;
+    }
+    return;
+  }
+  if (threadIdx.x == 0) {
+    const TokenOut o = token_math(a, row, zy, lse2, row_scale(a));
+    a.lp_out[row] = o.lp;
+    a.loss_tok[row] = o.loss;
+    if (a.flags) a.flags[row] = o.flags;
+    count_stats(a, o.flags);
+    bc->w = o.w;
+    bc->lse2 = lse2;
+    bc->dy = o.dy;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Register-resident row kernel, bf16 logits. NT threads x NC 16-byte chunks per thread;
+// thread tid owns chunks c * NT + tid. All row traffic goes through raw buffer accesses:
+// one VGPR offset per thread, the chunk offset c * NT * 16 in an SGPR.
+// ---------------------------------------------------------------------------------------
+template <int NT, int NC, bool BWD>
+__global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
+  __shared__ float red[2 * (NT / 64) + 2];
+  __shared__ Bcast bc;
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int V = a.V;
+  const int nfull = V >> 3;                 // 16-byte chunks fully inside the row
+  const bool loss_mode = a.mode != kModeLogprob;
+  const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
+  const int64_t y = a.ids[row];
+  const bool good = (y >= 0) && (y < V);
+  if (loss_mode && !(valid && good)) {
+    skip_row_resident<NT, NC, 2>(a, row, valid);
+    return;
+  }
+  const uint16_t* zrow = (const uint16_t*)a.logits + row * a.ld;
+  float zy = 0.0f;
+  if (tid == 0 && good) zy = bf16_to_f32(zrow[y]);
+
+  const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, V * 2);
+  const int voff = tid * 16;
+  uint32_t r[NC][4];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const u32x4 v = buf_load16(rz, voff, c * NT * 16);
+    r[c][0] = v.x; r[c][1] = v.y; r[c][2] = v.z; r[c][3] = v.w;
+  }
+  // Slots that can run past the last full chunk: pad with -inf (uniform test per slot).
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if ((c + 1) * NT > nfull && c * NT + tid >= nfull) {
+      r[c][0] = r[c][1] = r[c][2] = r[c][3] = kBf16NegInfPair;
+    }
+  }
+  // Ragged tail (V % 8 != 0): the chunk's owner reloads its elements one by one.
+  const int tail_slot = nfull / NT;
+  const bool tail_owner = (V & 7) != 0 && tid == nfull % NT;
+  if (tail_owner) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if (c == tail_slot) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int e = nfull * 8 + j;
+          if (e < V) {
+            const uint32_t h = zrow[e];
+            const int k = j >> 1;
+            r[c][k] = (j & 1) ? ((r[c][k] & 0x0000FFFFu) | (h << 16)) : ((r[c][k] & 0xFFFF0000u) | h);
+          }
+        }
+      }
+    }
+  }
+
+  // Pass 1: the thread's maximum.
+  float m = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) m = max3(m, bf16_lo(r[c][k]), bf16_hi(r[c][k]));
+
+  // Keep the packed words as the only live copy of the row: without this barrier the
+  // compiler reuses the unpacked floats of pass 1 in pass 2 and spills them.
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) asm volatile("" : "+v"(r[c][k]));
+
+  // Pass 2: sum of 2^(zL - n); the exponentials replace the logits as fp16 pairs.
+  const float n_shift = (m == -INFINITY) ? 0.0f : m * kLog2e;
+  const float nb = -n_shift;
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    float e[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      e[2 * k] = exp2_hw(__builtin_fmaf(bf16_lo(r[c][k]), kLog2e, nb));
+      e[2 * k + 1] = exp2_hw(__builtin_fmaf(bf16_hi(r[c][k]), kLog2e, nb));
+    }
+    s0 += e[0] + e[1];
+    s1 += e[2] + e[3];
+    s2 += e[4] + e[5];
+    s3 += e[6] + e[7];
+    if (BWD) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[c][k] = pack_f16(e[2 * k], e[2 * k + 1]);
+    }
+  }
+  if (BWD) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) asm volatile("" : "+v"(r[c][k]));
+  }
+  float n = (m == -INFINITY) ? -INFINITY : n_shift;
+  float s = (s0 + s1) + (s2 + s3);
+  const float n_mine = n;
+  block_merge_ns<NT>(n, s, red);
+  // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
+  const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+
+  finish_row(a, row, zy, lse2, good, &bc);
+  if (!BWD || !a.dlogits) return;
+  __syncthreads();
+  const float w = bc.w;
+  const float dy = bc.dy;
+  // softmax(z)[v] = e_v * 2^(n_mine - lse2). A thread whose elements are all -inf holds
+  // zeros; a NaN lse (non-finite row) makes every element NaN, as 0 * NaN does.
+  const float f = row_factor(w, n_mine, bc.lse2);
+
+  uint16_t* drow = (uint16_t*)a.dlogits + row * a.ldd;
+  const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, V * 2);
+  const int cy = (int)(y >> 3);
+  const int my_slot = (cy % NT == tid) ? cy / NT : -1;
+  const int jy = (int)(y & 7);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int idx = c * NT + tid;
+    float o[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      o[2 * k] = f16_lo_mul(r[c][k], f);
+      o[2 * k + 1] = f16_hi_mul(r[c][k], f);
+    }
+    if (c == my_slot) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = (j == jy) ? dy : o[j];
+    }
+    if ((c + 1) * NT <= nfull || idx < nfull) {
+      u32x4 v;
+      v.x = pack_bf16(o[0], o[1]);
+      v.y = pack_bf16(o[2], o[3]);
+      v.z = pack_bf16(o[4], o[5]);
+      v.w = pack_bf16(o[6], o[7]);
+      buf_store16_nt(v, rd, voff, c * NT * 16);
+    } else if (tail_owner && c == tail_slot) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = nfull * 8 + j;
+        if (e < V) drow[e] = to_bf16(o[j]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Register-resident row kernel, fp32 logits (4 per 16-byte chunk; exps stored as fp32).
+// ---------------------------------------------------------------------------------------
+template <int NT, int NC, bool BWD>
+__global__ __launch_bounds__(NT) void rows_f32_resident(RowArgs a) {
+  __shared__ float red[2 * (NT / 64) + 2];
+  __shared__ Bcast bc;
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int V = a.V;
+  const int nfull = V >> 2;
+  const bool loss_mode = a.mode != kModeLogprob;
+  const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
+  const int64_t y = a.ids[row];
+  const bool good = (y >= 0) && (y < V);
+  if (loss_mode && !(valid && good)) {
+    skip_row_resident<NT, NC, 4>(a, row, valid);
+    return;
+  }
+  const float* zrow = (const float*)a.logits + row * a.ld;
+  float zy = 0.0f;
+  if (tid == 0 && good) zy = zrow[y];
+
+  const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, V * 4);
+  const int voff = tid * 16;
+  float r[NC][4];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const u32x4 v = buf_load16(rz, voff, c * NT * 16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[c][j] = __uint_as_float(v[j]);
+  }
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if ((c + 1) * NT > nfull && c * NT + tid >= nfull) {
+      r[c][0] = r[c][1] = r[c][2] = r[c][3] = -INFINITY;
+    }
+  }
+  const int tail_slot = nfull / NT;
+  const bool tail_owner = (V & 3) != 0 && tid == nfull % NT;
+  if (tail_owner) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if (c == tail_slot) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int e = nfull * 4 + j;
+          if (e < V) r[c][j] = zrow[e];
+        }
+      }
+    }
+  }
+
+  float m = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    m = max3(m, r[c][0], r[c][1]);
+    m = max3(m, r[c][2], r[c][3]);
+  }
+  const float n_shift = (m == -INFINITY) ? 0.0f : m * kLog2e;
+  const float nb = -n_shift;
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    float e[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e[j] = exp2_hw(__builtin_fmaf(r[c][j], kLog2e, nb));
+    s0 += e[0]; s1 += e[1]; s2 += e[2]; s3 += e[3];
+    if (BWD) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r[c][j] = e[j];
+    }
+  }
+  float n = (m == -INFINITY) ? -INFINITY : n_shift;
+  float s = (s0 + s1) + (s2 + s3);
+  const float n_mine = n;
+  block_merge_ns<NT>(n, s, red);
+  const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+
+  finish_row(a, row, zy, lse2, good, &bc);
+  if (!BWD || !a.dlogits) return;
+  __syncthreads();
+  const float w = bc.w;
+  const float dy = bc.dy;
+  const float f = row_factor(w, n_mine, bc.lse2);
+  float* drow = (float*)a.dlogits + row * a.ldd;
+  const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, V * 4);
+  const int cy = (int)(y >> 2);
+  const int my_slot = (cy % NT == tid) ? cy / NT : -1;
+  const int jy = (int)(y & 3);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int idx = c * NT + tid;
+    float o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] = r[c][j] * f;
+    if (c == my_slot) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = (j == jy) ? dy : o[j];
+    }
+    if ((c + 1) * NT <= nfull || idx < nfull) {
+      const u32x4 v = {__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                       __float_as_uint(o[3])};
+      buf_store16_nt(v, rd, voff, c * NT * 16);
+    } else if (tail_owner && c == tail_slot) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int e = nfull * 4 + j;
+        if (e < V) drow[e] = o[j];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Streaming row kernel: any V, any alignment. Pass A reads the row once for (n, s); pass
+// B reads it again to write dlogits. Element e of the row is read and written by the same
+// thread, so dlogits may alias the logits.
+// ---------------------------------------------------------------------------------------
+template <typename Tin>
+__device__ __forceinline__ float load_elem(const Tin* p, int64_t i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, int64_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int64_t i) {
+  return bf16_to_f32(p[i]);
+}
+template <typename Tin>
+__device__ __forceinline__ void store_elem(Tin* p, int64_t i, float x);
+template <>
+__device__ __forceinline__ void store_elem<float>(float* p, int64_t i, float x) { p[i] = x; }
+template <>
+__device__ __forceinline__ void store_elem<uint16_t>(uint16_t* p, int64_t i, float x) {
+  p[i] = to_bf16(x);
+}
+
+// E elements per chunk: 16-byte vectors when VEC, single elements otherwise.
+template <typename Tin, bool VEC>
+struct Chunk {
+  static constexpr int E = VEC ? (int)(16 / sizeof(Tin)) : 1;
+  __device__ static void load(const Tin* row, int idx, int V, float (&x)[E]) {
+    if constexpr (VEC) {
+      if ((idx + 1) * E <= V) {
+        const u32x4 v = ((const u32x4*)row)[idx];
+        if constexpr (sizeof(Tin) == 2) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            x[2 * k] = bf16_lo(v[k]);
+            x[2 * k + 1] = bf16_hi(v[k]);
+          }
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) x[k] = __uint_as_float(v[k]);
+        }
+        return;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int e = idx * E + j;
+      x[j] = e < V ? load_elem<Tin>(row, e) : -INFINITY;
+    }
+  }
+  __device__ static void store(Tin* row, int idx, int V, const float (&o)[E]) {
+    if constexpr (VEC) {
+      if ((idx + 1) * E <= V) {
+        u32x4 v;
+        if constexpr (sizeof(Tin) == 2) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = pack_bf16(o[2 * k], o[2 * k + 1]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) v[k] = __float_as_uint(o[k]);
+        }
+        __builtin_nontemporal_store(v, ((u32x4*)row) + idx);
+        return;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int e = idx * E + j;
+      if (e < V) store_elem<Tin>(row, e, o[j]);
+    }
+  }
+};
+
+template <typename Tin, int NT, bool BWD, bool VEC>
+__global__ __launch_bounds__(NT) void rows_stream(RowArgs a) {
+  using C = Chunk<Tin, VEC>;
+  constexpr int E = C::E;
+  __shared__ float red[2 * (NT / 64) + 2];
+  __shared__ Bcast bc;
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int V = a.V;
+  const int nchunk = (V + E - 1) / E;
+  const bool loss_mode = a.mode != kModeLogprob;
+  const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
+  const int64_t y = a.ids[row];
+  const bool good = (y >= 0) && (y < V);
+  if (loss_mode && !(valid && good)) {
+    skip_row<Tin, NT>(a, row, valid);
+    return;
+  }
+  const Tin* zrow = (const Tin*)a.logits + row * a.ld;
+  float zy = 0.0f;
+  if (tid == 0 && good) zy = load_elem<Tin>(zrow, y);
+
+  float n = -INFINITY, s = 0.0f;
+  for (int idx = tid; idx < nchunk; idx += NT) {
+    float x[E];
+    C::load(zrow, idx, V, x);
+    float m = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < E; ++j) m = fmaxf(m, x[j]);
+    const float ns = (m == -INFINITY) ? 0.0f : m * kLog2e;
+    float cs = 0.0f;
+#pragma unroll
+    for (int j = 0; j < E; ++j) cs += exp2_hw(__builtin_fmaf(x[j], kLog2e, -ns));
+    merge_ns(n, s, (m == -INFINITY) ? -INFINITY : ns, cs);
+  }
+  block_merge_ns<NT>(n, s, red);
+  const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+
+  finish_row(a, row, zy, lse2, good, &bc);
+  if (!BWD || !a.dlogits) return;
+  __syncthreads();
+  const float w = bc.w;
+  const float dy = bc.dy;
+  const float nl = -bc.lse2;
+  Tin* drow = (Tin*)a.dlogits + row * a.ldd;
+  for (int idx = tid; idx < nchunk; idx += NT) {
+    float x[E];
+    C::load(zrow, idx, V, x);
+    float o[E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      o[j] = w * exp2_hw(__builtin_fmaf(x[j], kLog2e, nl));
+      if ((int64_t)idx * E + j == y) o[j] = dy;
+    }
+    C::store(drow, idx, V, o);
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Valid-token count (prepares stats for the token-mean scale) and the loss sum.
+// ---------------------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void prep_stats(const uint8_t* mask, int64_t T, int32_t* stats) {
+  __shared__ int part[16];
+  int cnt = 0;
+  if (mask) {
+    for (int64_t i = threadIdx.x; i < T; i += 1024) cnt += mask[i] != 0;
+  } else if (threadIdx.x == 0) {
+    cnt = (int)T;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int tot = 0;
+    for (int i = 0; i < 16; ++i) tot += part[i];
+    stats[DPPO_STAT_N_VALID] = tot;
+    stats[DPPO_STAT_N_BAND] = 0;
+    stats[DPPO_STAT_N_PPO] = 0;
+    stats[DPPO_STAT_N_ACTIVE] = 0;
+    stats[DPPO_STAT_N_BAD] = 0;
+  }
+}
+
+// L = sum_t m_t s_t l_t in float64, each thread over a fixed stride, then a fixed tree:
+// the same inputs give the same bits on every run.
+__global__ __launch_bounds__(1024) void loss_sum(const float* loss_tok, const uint8_t* mask,
+                                                 const float* tscale, const int32_t* stats,
+                                                 int64_t T, float loss_scale, int32_t scale_mode,
+                                                 float* loss_out) {
+  __shared__ double part[16];
+  float scale = loss_scale;
+  if (scale_mode == DPPO_SCALE_TOKEN_MEAN) {
+    const int n = stats[DPPO_STAT_N_VALID];
+    scale = loss_scale / (float)(n > 1 ? n : 1);
+  }
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < T; i += 1024) {
+    if (mask && mask[i] == 0) continue;
+    const float s = scale * (tscale ? tscale[i] : 1.0f);
+    acc += (double)s * (double)loss_tok[i];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+    for (int i = 0; i < 16; ++i) tot += part[i];
+    loss_out[0] = (float)tot;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Kernel selection.
+// ---------------------------------------------------------------------------------------
+namespace {
+struct ResCfg {
+  int nt, nc;
+};
+// Resident shapes, by capacity in 16-byte chunks (NT * NC).
+constexpr ResCfg kResident[] = {{256, 1},  {256, 2},  {256, 4},   {512, 4},   {512, 6},  {512, 8},
+                                {1024, 6}, {1024, 8}, {1024, 12}, {1024, 16}, {1024, 19}};
+constexpr int kNumResident = sizeof(kResident) / sizeof(kResident[0]);
+
+template <bool BWD>
+RowKernel pick_bf16(int i) {
+  switch (i) {
+    case 0: return rows_bf16_resident<256, 1, BWD>;
+    case 1: return rows_bf16_resident<256, 2, BWD>;
+    case 2: return rows_bf16_resident<256, 4, BWD>;
+    case 3: return rows_bf16_resident<512, 4, BWD>;
+    case 4: return rows_bf16_resident<512, 6, BWD>;
+    case 5: return rows_bf16_resident<512, 8, BWD>;
+    case 6: return rows_bf16_resident<1024, 6, BWD>;
+    case 7: return rows_bf16_resident<1024, 8, BWD>;
+    case 8: return rows_bf16_resident<1024, 12, BWD>;
+    case 9: return rows_bf16_resident<1024, 16, BWD>;
+    default: return rows_bf16_resident<1024, 19, BWD>;
+  }
+}
+template <bool BWD>
+RowKernel pick_f32(int i) {
+  switch (i) {
+    case 0: return rows_f32_resident<256, 1, BWD>;
+    case 1: return rows_f32_resident<256, 2, BWD>;
+    case 2: return rows_f32_resident<256, 4, BWD>;
+    case 3: return rows_f32_resident<512, 4, BWD>;
+    case 4: return rows_f32_resident<512, 6, BWD>;
+    case 5: return rows_f32_resident<512, 8, BWD>;
+    case 6: return rows_f32_resident<1024, 6, BWD>;
+    case 7: return rows_f32_resident<1024, 8, BWD>;
+    case 8: return rows_f32_resident<1024, 12, BWD>;
+    case 9: return rows_f32_resident<1024, 16, BWD>;
+    default: return rows_f32_resident<1024, 19, BWD>;
+  }
+}
+}  // namespace
+
+RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force) {
+  RowLaunch L;
+  const int esize = dtype == DPPO_BF16 ? 2 : 4;
+  const int64_t chunks = (V * esize + 15) / 16;
+  int pick = -1;
+  if (aligned && force != kForceStream) {
+    for (int i = 0; i < kNumResident; ++i) {
+      if ((int64_t)kResident[i].nt * kResident[i].nc >= chunks) {
+        pick = i;
+        break;
+      }
+    }
+  }
+  if (pick >= 0) {
+    L.threads = kResident[pick].nt;
+    L.fn = dtype == DPPO_BF16 ? (bwd ? pick_bf16<true>(pick) : pick_bf16<false>(pick))
+                              : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
+    L.resident = true;
+    return L;
+  }
+  L.threads = 1024;
+  L.resident = false;
+  if (dtype == DPPO_BF16) {
+    L.fn = aligned ? (bwd ? rows_stream<uint16_t, 1024, true, true> : rows_stream<uint16_t, 1024, false, true>)
+                   : (bwd ? rows_stream<uint16_t, 1024, true, false> : rows_stream<uint16_t, 1024, false, false>);
+  } else {
+    L.fn = aligned ? (bwd ? rows_stream<float, 1024, true, true> : rows_stream<float, 1024, false, true>)
+                   : (bwd ? rows_stream<float, 1024, true, false> : rows_stream<float, 1024, false, false>);
+  }
+  return L;
+}
+
+void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream_t st) {
+  prep_stats<<<1, 1024, 0, st>>>(mask, T, stats);
+}
+
+void launch_loss_sum(const float* loss_tok, const uint8_t* mask, const float* tscale,
+                     const int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
+                     float* loss_out, hipStream_t st) {
+  loss_sum<<<1, 1024, 0, st>>>(loss_tok, mask, tscale, stats, T, loss_scale, scale_mode, loss_out);
+}
+
+}  // namespace dppo

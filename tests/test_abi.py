@@ -1,0 +1,181 @@
+"""Host-side checks of the C ABI: the library loads, exports every function that
+include/dppo.h declares, and rejects bad arguments before touching the GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2605_12070_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dppo.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(_lib.LIB_PATH),
+                                reason="libdppo.so not built")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = re.sub(r"#[^\n]*", "", src)
+    names = []
+    for stmt in src.split(";"):
+        stmt = " ".join(stmt.split())
+        if "(" not in stmt or stmt.startswith("typedef") or "{" in stmt:
+            continue
+        m = re.search(r"(\w+)\s*\(", stmt)
+        if m:
+            names.append(m.group(1))
+    return names
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "ewma_proxy_update",
+                     "dppo_strerror"):
+        assert required in names
+    assert set(names) == set(_lib.SIGNATURES), "binding signatures out of sync with the header"
+
+
+def test_library_exports_every_declared_symbol():
+    h = C.CDLL(_lib.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(h, name), name
+    assert _lib.lib().dppo_abi_version() == _lib.ABI_VERSION
+
+
+def test_strerror():
+    L = _lib.lib()
+    assert L.dppo_strerror(0) == b"success"
+    assert b"invalid" in L.dppo_strerror(1)
+    assert L.dppo_strerror(99) == b"unknown status"
+
+
+FAKE = 0x10000  # never dereferenced: every case below fails its host-side check first
+
+
+def _params(**kw):
+    d = dict(band_lo=0.5, band_hi=2.0, clip_eps_lo=0.2, clip_eps_hi=0.2, rd_mode=3,
+             scale_mode=1, loss_scale=1.0)
+    d.update(kw)
+    return _lib.DppoParams(**d)
+
+
+def _loss(T=4, V=8, ld=8, dtype=1, p=None, dl=None, ldd=8, ids=FAKE, logits=FAKE, stats=FAKE,
+          loss=FAKE):
+    p = p or _params()
+    L = _lib.lib()
+    return L.decoupled_ppo_loss_fwd_bwd(logits, dtype, T, V, ld, ids, FAKE, FAKE, FAKE, None,
+                                        None, C.byref(p), FAKE, FAKE, loss, None, dl, ldd,
+                                        stats, None)
+
+
+@pytest.mark.parametrize("kw,frag", [
+    (dict(dtype=7), "dtype"),
+    (dict(T=-1), "T ="),
+    (dict(V=0), "V ="),
+    (dict(ld=4), "stride"),
+    (dict(ids=None), "required"),
+    (dict(logits=None), "NULL"),
+    (dict(stats=None), "required"),
+    (dict(loss=None), "required"),
+    (dict(p=_params(band_lo=3.0)), "band"),
+    (dict(p=_params(band_lo=float("nan"))), "band"),
+    (dict(p=_params(band_lo=-0.5)), "band"),
+    (dict(p=_params(clip_eps_lo=-0.1)), "clip"),
+    (dict(p=_params(clip_eps_hi=float("inf"))), "clip"),
+    (dict(p=_params(loss_scale=float("nan"))), "loss_scale"),
+    (dict(p=_params(rd_mode=9)), "rd_mode"),
+    (dict(p=_params(scale_mode=5)), "scale_mode"),
+    (dict(dl=FAKE + 2 * 8, ldd=8), "overlaps"),        # dlogits overlaps logits, not equal
+    (dict(dl=FAKE, ldd=16, ld=8), "overlaps"),          # same base, different stride
+    (dict(dl=FAKE + 64, ldd=4), "stride"),
+])
+def test_loss_rejects_bad_arguments(kw, frag):
+    st = _loss(**kw)
+    assert st == _lib.DPPO_ERR_INVALID_ARG
+    assert frag in _lib.lib().dppo_last_error().decode()
+
+
+def test_loss_null_params():
+    L = _lib.lib()
+    st = L.decoupled_ppo_loss_fwd_bwd(FAKE, 1, 4, 8, 8, FAKE, FAKE, FAKE, FAKE, None, None,
+                                      None, FAKE, FAKE, FAKE, None, None, 0, FAKE, None)
+    assert st == _lib.DPPO_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("args,frag", [
+    ((FAKE, 5, 4, 8, 8, FAKE, FAKE, None, None), "dtype"),
+    ((FAKE, 1, 4, 8, 7, FAKE, FAKE, None, None), "stride"),
+    ((FAKE, 1, 4, 8, 8, None, FAKE, None, None), "required"),
+    ((FAKE, 1, 4, 8, 8, FAKE, None, None, None), "required"),
+    ((FAKE, 1, 1 << 31, 8, 8, FAKE, FAKE, None, None), "T ="),
+])
+def test_logprob_rejects_bad_arguments(args, frag):
+    st = _lib.lib().logprob_fwd(*args)
+    assert st == _lib.DPPO_ERR_INVALID_ARG
+    assert frag in _lib.lib().dppo_last_error().decode()
+
+
+def test_logprob_empty_batch_is_a_no_op():
+    # T = 0 enqueues nothing, so it is safe without a GPU
+    assert _lib.lib().logprob_fwd(None, 1, 0, 8, 8, None, None, None, None) == _lib.DPPO_OK
+
+
+@pytest.mark.parametrize("kw,frag", [
+    (dict(dtype=3), "dtype"),
+    (dict(n=-1), "n ="),
+    (dict(beta=1.0), "beta"),
+    (dict(beta=-0.1), "beta"),
+    (dict(beta=float("nan")), "beta"),
+    (dict(xp=None), "required"),
+    (dict(w=None), "w is required"),
+    (dict(w=-1.0), "w_{t-1}"),
+    (dict(xn=FAKE + 8), "overlaps"),
+])
+def test_ewma_rejects_bad_arguments(kw, frag):
+    d = dict(xp=FAKE, xn=FAKE + 4096, dtype=0, n=16, beta=0.5, w=0.0, reset=0, normalized=1)
+    d.update(kw)
+    wref = None if d["w"] is None else C.byref(C.c_double(d["w"]))
+    st = _lib.lib().ewma_proxy_update(d["xp"], d["xn"], d["dtype"], d["n"], d["beta"], wref,
+                                      d["reset"], d["normalized"], None)
+    assert st == _lib.DPPO_ERR_INVALID_ARG
+    assert frag in _lib.lib().dppo_last_error().decode()
+
+
+def test_ewma_empty_buffer_updates_w_only():
+    w = C.c_double(0.0)
+    L = _lib.lib()
+    assert L.ewma_proxy_update(None, None, 0, 0, 0.5, C.byref(w), 0, 1, None) == _lib.DPPO_OK
+    assert w.value == 1.0
+    assert L.ewma_proxy_update(None, None, 0, 0, 0.5, C.byref(w), 0, 1, None) == _lib.DPPO_OK
+    assert w.value == 1.5
+    assert L.ewma_proxy_update(None, None, 0, 0, 0.5, C.byref(w), 1, 1, None) == _lib.DPPO_OK
+    assert w.value == 1.0
+
+
+def test_path_policy_validation():
+    L = _lib.lib()
+    assert L.dppo_set_path_policy(2) == _lib.DPPO_ERR_INVALID_ARG
+    assert L.dppo_set_path_policy(0) == _lib.DPPO_OK
+
+
+def test_timer_read_requires_outputs():
+    assert _lib.lib().dppo_timer_read(None, None) == _lib.DPPO_ERR_INVALID_ARG
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        _lib.lib()
+
+
+def test_host_controller_logic():
+    import paper_2605_12070_amd as P
+    assert P.beta_from_window(6) == 0.75 and P.beta_from_window(2) == 0.5
+    assert P.train_infer_mask_value([10, 9, 9, 8, 0]) == 0.8
+    assert P.train_infer_mask_value([0, 0, 0, 0, 0]) == 1.0
+    assert abs(P.ppo_clip_ratio([10, 9, 7, 6, 0]) - 0.3) < 1e-12

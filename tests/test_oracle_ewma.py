@@ -1,4 +1,4 @@
-"""Pins of the oracle's PPO-EWMA proxy (Sec. 4.2, Eq. 5; App. B) and reset rule."""
+"""Pins of the oracle's PPO-EWMA proxy (Sec. 5.2, Eq. 5; App. B) and reset rule."""
 import numpy as np
 import pytest
 

@@ -1,0 +1,88 @@
+"""Full-size parity: the large-vocabulary (T=16384, V=151936, bf16) and long-agentic
+(T=65536, 40% masked) workloads, run exactly as the benchmark runs them. The oracle checks
+a sample of rows (random rows plus the rows nearest to a threshold); properties that hold
+at any size check every row."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_12070_amd as P
+from paper_2605_12070_amd import workloads as W
+
+from helpers import bits_of, compare_loss, oracle_params, torch_anchor
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _sample_rows(res_flags, ref_lp_ref, lp_mu, gpu_lp, n_rand, seed, T, mask):
+    rng = np.random.default_rng(seed)
+    valid = np.nonzero(mask)[0]
+    rows = set(rng.choice(valid, size=min(n_rand, valid.size), replace=False).tolist())
+    rows |= {int(valid[0]), int(valid[-1])}
+    # rows whose GPU ratios sit closest to a threshold
+    ls = gpu_lp - ref_lp_ref
+    ld = ref_lp_ref - lp_mu
+    th = np.log([0.8, 1.2, 0.5, 2.0])
+    dist = np.minimum(np.min(np.abs(ls[:, None] - th[None, :2]), 1),
+                      np.min(np.abs(ld[:, None] - th[None, 2:]), 1))
+    dist[~mask.astype(bool)] = np.inf
+    rows |= set(np.argsort(dist)[:16].tolist())
+    return np.array(sorted(rows))
+
+
+def _check_workload(wl, lp_ref, lp_mu, oracle_lp_ref, n_rand=48):
+    """lp_ref feeds the kernel; oracle_lp_ref (host, float64) feeds the oracle."""
+    T, V = wl.T, wl.V
+    print(f"[case] fullsize {wl.name} T={T} V={V}", flush=True)
+    res = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask)
+    torch.cuda.synchronize()
+    mask = wl.mask.cpu().numpy()
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    scale = oracle.batch_scale(mask, params)
+    rows = _sample_rows(res.flags.cpu().numpy(), oracle_lp_ref,
+                        lp_mu.cpu().double().numpy(), res.logp.cpu().double().numpy(),
+                        n_rand, 0, T, mask)
+    idx = torch.as_tensor(rows, device=DEV)
+    ref = oracle.per_token(bits_of(wl.logits[idx]), wl.ids[idx].cpu().numpy(),
+                           lp_mu[idx].cpu().double().numpy(), oracle_lp_ref[rows],
+                           wl.adv[idx].cpu().double().numpy(), mask[rows], None, params, scale)
+    compare_loss(res, ref, params, wl.logits.dtype, rows=rows)
+
+    # properties on every row
+    fl = res.flags.cpu().numpy()
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
+    assert st[0] == int(mask.sum())
+    lt = res.loss_tok.cpu().double().numpy()
+    own = float(np.sum(np.where(mask != 0, scale * lt, 0.0)))
+    assert abs(res.loss.item() - own) <= 1e-6 * (np.sum(np.abs(scale * lt)) + 1e-30)
+    # each dlogits row sums to ~0 (softmax sums to one); masked rows are exactly zero
+    for a in range(0, T, 2048):
+        d = res.dlogits[a:a + 2048].float()
+        rs = d.sum(1).abs()
+        mag = d.abs().sum(1)
+        assert torch.all(rs <= 2.0 ** -7 * mag + 1e-20), "row sums"
+        m = wl.mask[a:a + 2048] == 0
+        assert torch.all(mag[m] == 0)
+    return res
+
+
+def test_large_vocab_fullsize():
+    wl = W.make_workload("large_vocab", device=DEV)
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    _check_workload(wl, lp_ref, lp_mu, lp_ref.cpu().double().numpy())
+
+
+def test_long_agentic_fullsize():
+    wl = W.make_workload("long_agentic", device=DEV)
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_old, lp_prev, lp_mu = W.version_logprobs(anchor, wl)
+    prox = lp_prev.clone()
+    P.ewma_proxy_update(prox, lp_old, 0.9, normalized=False)
+    # the oracle forms its own proxy from the same two versions' log-probs
+    ref_prox = oracle.ewma_fixed_step(lp_prev.cpu().double().numpy(),
+                                      lp_old.cpu().double().numpy(), 0.9)
+    _check_workload(wl, prox, lp_mu, ref_prox)

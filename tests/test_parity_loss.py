@@ -1,0 +1,309 @@
+"""GPU parity of decoupled_ppo_loss_fwd_bwd (through the C ABI) against the float64 oracle.
+
+Every case prints its name, shape and seed before it touches the GPU.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_12070_amd as P
+from paper_2605_12070_amd import workloads as W
+
+from helpers import (bits_of, compare_loss, oracle_anchor, oracle_params, run_oracle,
+                     tie_mask)
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _run_case(wl_name, T=None, V=None, seed=None, seq_len=None, rd_mode="mask_weight",
+              scale_mode="token_mean", loss_scale=1.0, band=(0.5, 2.0), eps=(0.2, 0.2),
+              tscale=False, policy="auto", check_loss=True):
+    _say(wl_name, T, V, seed, rd_mode, scale_mode, loss_scale, band, eps, tscale, policy)
+    wl = W.make_workload(wl_name, device=DEV, T=T, V=V, seed=seed, seq_len=seq_len)
+    anchor = oracle_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor.to(DEV), wl)
+    ts = None
+    if tscale:
+        g = torch.Generator(device=DEV).manual_seed(99)
+        ts = torch.rand(wl.T, generator=g, device=DEV) * 1.5 + 0.25
+    P.set_path_policy(policy)
+    try:
+        res = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask, ts,
+                                           band=band, clip_eps=eps, rd_mode=rd_mode,
+                                           scale_mode=scale_mode, loss_scale=loss_scale)
+        torch.cuda.synchronize()
+    finally:
+        P.set_path_policy("auto")
+    params = oracle_params(band, eps, rd_mode, scale_mode, loss_scale)
+    ref = run_oracle(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask, ts, params)
+    n_ties = compare_loss(res, ref, params, wl.logits.dtype)
+    # stats: consistent with the kernel's own flags, equal to the oracle's without ties
+    fl = res.flags.cpu().numpy()
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
+    if n_ties == 0:
+        np.testing.assert_array_equal(st, ref["stats"])
+    if check_loss:
+        denom = np.nansum(np.abs(np.where(ref["valid"], ref["s"] * ref["loss_tok"], 0.0))) + 1e-30
+        if n_ties == 0:
+            assert abs(res.loss.item() - ref["loss"]) <= 1e-5 * denom + 1e-30, \
+                (res.loss.item(), ref["loss"])
+        # the loss is the fixed-order sum of the kernel's own per-token values
+        lt = res.loss_tok.cpu().double().numpy()
+        s = ref["s"]
+        own = float(np.sum(np.where(ref["valid"], s * lt, 0.0)))
+        assert abs(res.loss.item() - own) <= 1e-6 * denom + 1e-30
+    return wl, res, ref
+
+
+@pytest.mark.parametrize("rd_mode", ["none", "mask", "weight", "mask_weight"])
+@pytest.mark.parametrize("scale_mode", ["const", "token_mean"])
+def test_tiny_fp32_all_modes(rd_mode, scale_mode):
+    _run_case("tiny", rd_mode=rd_mode, scale_mode=scale_mode)
+
+
+def test_tiny_fp32_token_scale_asymmetric_clip():
+    _run_case("tiny", tscale=True, eps=(0.1, 0.3), scale_mode="const", loss_scale=0.5)
+
+
+def test_tiny_stream_path_matches():
+    _run_case("tiny", policy="stream")
+
+
+@pytest.mark.parametrize("policy", ["auto", "stream"])
+def test_small_vocab_bf16(policy):
+    # 2 sequences of the 32000-vocabulary workload: spiked rows and +-1 lp_mu offsets
+    _run_case("small_vocab", T=512, policy=policy)
+
+
+def test_small_vocab_unit_scale_dlogits():
+    # loss_scale = 1 makes dlogits O(1), so the relative bf16 bound is exercised
+    _run_case("small_vocab", T=256, scale_mode="const", loss_scale=1.0)
+
+
+@pytest.mark.parametrize("rd_mode", ["mask_weight", "weight"])
+def test_large_vocab_full_rows(rd_mode):
+    # full V = 151936: the 1024-thread x 19-chunk register-resident kernel
+    _run_case("large_vocab", T=64, seq_len=8, rd_mode=rd_mode)
+
+
+def test_large_vocab_unit_scale():
+    _run_case("large_vocab", T=32, seq_len=4, scale_mode="const", loss_scale=1.0)
+
+
+def test_large_vocab_paper_thresholds():
+    # thresholds of the paper's threshold study (snap1003_1006) and Table 4's first row:
+    # dense decisions near 1
+    _run_case("large_vocab", T=64, seq_len=8, band=(1 / 1.003, 1.003), eps=(0.006, 0.006))
+    _run_case("large_vocab", T=64, seq_len=8, band=(0.990, 1.010), eps=(0.003, 0.004))
+
+
+def test_large_vocab_stream_path():
+    _run_case("large_vocab", T=16, seq_len=2, policy="stream")
+
+
+def test_long_agentic_masked_with_ewma_reference():
+    # 40% observation tokens (mask 0), lp_ref = fixed-decay EWMA (beta = 0.9) of two
+    # versions' log-probs; the GPU leg forms the proxy with ewma_proxy_update, the oracle
+    # leg with its own recursion
+    T = 512
+    _say("long_agentic", T)
+    wl = W.make_workload("long_agentic", device=DEV, T=T)
+    anchor = oracle_anchor(wl.logits, wl.ids)
+    lp_old, lp_prev, lp_mu = W.version_logprobs(anchor.to(DEV), wl)
+    prox = lp_prev.clone()
+    P.ewma_proxy_update(prox, lp_old, 0.9, normalized=False)
+    ref_prox = oracle.ewma_fixed_step(lp_prev.cpu().double().numpy(),
+                                      lp_old.cpu().double().numpy(), 0.9)
+    np.testing.assert_allclose(prox.cpu().double().numpy(), ref_prox, rtol=1e-6, atol=1e-6)
+    res = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, prox, wl.adv, wl.mask)
+    torch.cuda.synchronize()
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    ref = oracle.decoupled_ppo_loss(bits_of(wl.logits), wl.ids.cpu().numpy(),
+                                    lp_mu.cpu().double().numpy(), ref_prox,
+                                    wl.adv.cpu().double().numpy(), wl.mask.cpu().numpy(),
+                                    params=params)
+    compare_loss(res, ref, params, wl.logits.dtype)
+    m = wl.mask.cpu().numpy() == 0
+    d = res.dlogits.cpu()
+    assert torch.all(d[torch.from_numpy(m)] == 0)
+    assert np.all(res.logp.cpu().numpy()[m] == 0) and np.all(res.flags.cpu().numpy()[m] == 0)
+    assert res.stats[0].item() == int((~m).sum())
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("V", [1, 7, 8, 9, 1000, 1023, 1025, 4097, 32001, 77824, 77825,
+                               151937, 155648, 155656])
+def test_ragged_vocab_sizes(dtype, V):
+    _say("ragged", dtype, V)
+    T = 6
+    g = torch.Generator(device=DEV).manual_seed(V)
+    z = (torch.randn(T, V, generator=g, device=DEV) * 3).to(dtype)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[0] = V - 1
+    ids[1] = 0
+    anchor = oracle_anchor(z, ids).to(DEV)
+    lp_ref = (anchor + 0.1 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.05 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    for policy in ("auto", "stream"):
+        P.set_path_policy(policy)
+        try:
+            res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, scale_mode="const")
+            torch.cuda.synchronize()
+        finally:
+            P.set_path_policy("auto")
+        params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+        ref = run_oracle(z, ids, lp_mu, lp_ref, adv, None, None, params)
+        compare_loss(res, ref, params, dtype)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_unaligned_and_strided_rows(dtype):
+    # base pointer off by one element and a row stride that is not a multiple of 16 bytes:
+    # the element-wise streaming path
+    T, V = 12, 5003
+    _say("unaligned", dtype, T, V)
+    ld = V + 3
+    g = torch.Generator(device=DEV).manual_seed(5)
+    buf = (torch.randn(T * ld + 1, generator=g, device=DEV) * 3).to(dtype)
+    z = buf[1:1 + T * ld].view(T, ld)[:, :V]
+    dbuf = torch.zeros(T * ld + 1, dtype=dtype, device=DEV)
+    d = dbuf[1:1 + T * ld].view(T, ld)[:, :V]
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    anchor = oracle_anchor(z, ids).to(DEV)
+    lp_ref = (anchor + 0.1 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = lp_ref.clone()
+    adv = torch.randn(T, generator=g, device=DEV)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, dlogits=d, scale_mode="const")
+    torch.cuda.synchronize()
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, None, None, params)
+    compare_loss(res, ref, params, dtype)
+    # the padding between rows and the element before the matrix are untouched
+    pad = dbuf[1:1 + T * ld].view(T, ld)[:, V:]
+    assert torch.all(pad == 0) and dbuf[0].item() == 0
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_in_place_dlogits(dtype):
+    T, V = 24, 32000
+    _say("in_place", dtype, T, V)
+    wl = W.make_workload("small_vocab", device=DEV, T=T, V=V, seed=7)
+    z = wl.logits.to(dtype)
+    anchor = oracle_anchor(z, wl.ids).to(DEV)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    out_of_place = P.decoupled_ppo_loss_fwd_bwd(z, wl.ids, lp_mu, lp_ref, wl.adv)
+    zz = z.clone()
+    in_place = P.decoupled_ppo_loss_fwd_bwd(zz, wl.ids, lp_mu, lp_ref, wl.adv, dlogits=zz)
+    torch.cuda.synchronize()
+    assert torch.equal(in_place.dlogits, out_of_place.dlogits)
+    assert in_place.dlogits.data_ptr() == zz.data_ptr()
+    assert torch.equal(in_place.logp, out_of_place.logp)
+
+
+def test_deterministic_bitwise():
+    wl = W.make_workload("small_vocab", device=DEV, T=1024, seed=11)
+    _say("determinism", wl.T, wl.V)
+    anchor = oracle_anchor(wl.logits, wl.ids).to(DEV)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    a = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv)
+    b = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv)
+    torch.cuda.synchronize()
+    for x, y in ((a.loss, b.loss), (a.dlogits, b.dlogits), (a.logp, b.logp), (a.stats, b.stats),
+                 (a.loss_tok, b.loss_tok), (a.flags, b.flags)):
+        assert torch.equal(x, y)
+
+
+def test_masked_rows_bad_ids_and_nonfinite_rows():
+    T, V = 10, 3000
+    _say("edge rows", T, V)
+    g = torch.Generator(device=DEV).manual_seed(3)
+    for dtype in (torch.float32, torch.bfloat16):
+        z = (torch.randn(T, V, generator=g, device=DEV) * 2).to(dtype)
+        ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+        z[2, 17] = float("nan")            # NaN row
+        z[3, 5] = float("inf")             # +inf row
+        z[4, :] = float("-inf")            # all -inf row
+        z[5, ::2] = float("-inf")          # some -inf entries
+        ids[5] = 1
+        z[6, :] = float("nan")             # masked: never read
+        ids[7] = V                         # bad id on a valid row
+        ids[8] = -5                        # bad id on a masked row
+        mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+        mask[6] = 0
+        mask[8] = 0
+        lp_ref = torch.full((T,), -8.0, device=DEV)
+        lp_mu = lp_ref.clone()
+        adv = torch.linspace(-1, 1, T, device=DEV)
+        for policy in ("auto", "stream"):
+            P.set_path_policy(policy)
+            try:
+                res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask,
+                                                   scale_mode="const")
+                torch.cuda.synchronize()
+            finally:
+                P.set_path_policy("auto")
+            params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+            ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+            compare_loss(res, ref, params, dtype)
+            st = res.stats.cpu().numpy()
+            assert st[P.STAT_N_VALID] == 8 and st[P.STAT_N_BAD] == 1
+            assert math.isnan(res.loss.item()) and math.isnan(ref["loss"])
+
+
+def test_empty_batch():
+    z = torch.zeros(0, 16, device=DEV)
+    e = torch.zeros(0, device=DEV)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, torch.zeros(0, dtype=torch.int64, device=DEV), e, e, e)
+    torch.cuda.synchronize()
+    assert res.loss.item() == 0.0 and res.stats.tolist() == [0, 0, 0, 0, 0]
+
+
+def test_worked_example_through_the_kernel():
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "loss_worked_example.json")))
+    z_row = [math.log(v) for v in g["logits_row"]["log_terms"]]
+    toks = g["tokens"]
+    T = len(toks)
+    z = torch.tensor([z_row] * T, dtype=torch.float32, device=DEV)
+    ids = torch.tensor([t["y"] for t in toks], device=DEV)
+    lpt = [math.log(g["lp_theta"][t["name"]][0]) for t in toks]
+    lp_ref = torch.tensor([a - math.log(t["r_s"]) for a, t in zip(lpt, toks)], device=DEV)
+    lp_mu = torch.tensor([a - math.log(t["r_s"]) - math.log(t["r_d"]) for a, t in zip(lpt, toks)],
+                         device=DEV)
+    adv = torch.tensor([t["adv"] for t in toks], device=DEV)
+    for mode, exp in g["modes"].items():
+        _say("worked example", mode)
+        res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, rd_mode=mode,
+                                           scale_mode="const")
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(res.loss_tok.cpu().numpy(), exp["loss_tok"], atol=2e-6)
+        np.testing.assert_allclose(res.dlogits.cpu().numpy(), np.array(exp["dlogits"]), atol=2e-6)
+        assert abs(res.loss.item() - exp["loss"]) < 1e-5
+        assert res.stats.cpu().tolist() == exp["stats"]
+
+
+def test_forward_only_and_autograd_wrapper():
+    wl = W.make_workload("tiny", device=DEV)
+    anchor = oracle_anchor(wl.logits, wl.ids).to(DEV)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    fwd = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, want_dlogits=False)
+    both = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv)
+    torch.cuda.synchronize()
+    assert fwd.dlogits is None
+    assert torch.equal(fwd.loss, both.loss) and torch.equal(fwd.logp, both.logp)
+    z = wl.logits.clone().requires_grad_(True)
+    loss, lp, st = P.DecoupledPPOLoss.apply(z, wl.ids, lp_mu, lp_ref, wl.adv, None, None, None)
+    (2.0 * loss).backward()
+    torch.cuda.synchronize()
+    assert torch.allclose(z.grad, 2.0 * both.dlogits, rtol=0, atol=0)
