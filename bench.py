@@ -186,7 +186,7 @@ def main():
     achieved = b_alg / (k_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                "kernel": "rows_bf16_resident<1024,19>" if esize == 2 else "row kernel",
+                "kernel": "rows_bf16_resident<512,38>" if esize == 2 else "row kernel",
                 "kernel_ms": round(k_ms, 4), "alg_bytes_per_launch": b_alg}
     if os.path.exists(TRAFFIC_FILE):
         try:

@@ -72,12 +72,44 @@ std::pair<hipEvent_t, hipEvent_t>* timer_slot() {
   return &g_timer.pool[g_timer.used++];
 }
 
+// Workgroups of `fn` that fit on the current device at once (CUs x per-CU occupancy),
+// cached per (device, kernel).
+hipError_t resident_slots(const dppo::RowLaunch& L, int64_t* slots) {
+  static std::mutex mu;
+  static std::vector<std::pair<std::pair<int, const void*>, int64_t>> cache;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  for (auto& kv : cache) {
+    if (kv.first.first == dev && kv.first.second == (const void*)L.fn) {
+      *slots = kv.second;
+      return hipSuccess;
+    }
+  }
+  int cus = 0, per_cu = 0;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)L.fn, L.threads, 0);
+  if (e != hipSuccess) return e;
+  *slots = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
+  cache.push_back({{dev, (const void*)L.fn}, *slots});
+  return hipSuccess;
+}
+
 dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgs& args, int64_t T,
                         hipStream_t st) {
+  int64_t grid = T;
+  if (L.persistent) {
+    int64_t slots = 0;
+    const hipError_t oe = resident_slots(L, &slots);
+    if (oe != hipSuccess) return hip_fail(oe, "occupancy query");
+    if (slots < grid) grid = slots;
+  }
   auto* ev = timer_slot();
   if (ev) (void)hipEventRecord(ev->first, st);
   void* kargs[] = {(void*)&args};
-  hipError_t e = hipLaunchKernel((const void*)L.fn, dim3((unsigned)T), dim3((unsigned)L.threads),
+  hipError_t e = hipLaunchKernel((const void*)L.fn, dim3((unsigned)grid), dim3((unsigned)L.threads),
                                  kargs, 0, st);
   if (e == hipSuccess) e = hipGetLastError();
   if (ev) (void)hipEventRecord(ev->second, st);
@@ -169,6 +201,7 @@ dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V,
   a.ids = token_ids;
   a.lp_out = logp_out;
   a.lse_out = lse_out;
+  a.T = (int32_t)T;
   a.V = (int32_t)V;
   a.mode = dppo::kModeLogprob;
   return launch_rows(L, a, T, (hipStream_t)stream);
@@ -228,6 +261,7 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
     a.loss_tok = loss_tok_out;
     a.flags = flags_out;
     a.stats = stats_out;
+    a.T = (int32_t)T;
     a.V = (int32_t)V;
     a.mode = dppo::kModeLoss;
     a.band_lo = p->band_lo;

@@ -126,8 +126,22 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int by
 __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
 }
+__device__ __forceinline__ void load16(uint32_t (&d)[4], __amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  d[0] = v.x;
+  d[1] = v.y;
+  d[2] = v.z;
+  d[3] = v.w;
+}
 __device__ __forceinline__ void buf_store16_nt(u32x4 v, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
   __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
+}
+
+// Load of a value at a workgroup-uniform address through the scalar unit (constant
+// address space): waited on with lgkmcnt, so it never waits behind the row's vector loads.
+template <typename T>
+__device__ __forceinline__ T uload(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
 }
 
 // numpy-style minimum: NaN if either operand is NaN.

@@ -29,6 +29,7 @@ struct RowArgs {
   uint8_t* flags;       // NULL: not written
   int32_t* stats;
   float* lse_out;       // log-prob mode only, may be NULL
+  int32_t T;            // rows (persistent kernels loop over them)
   int32_t V;
   int32_t mode;
   float band_lo, band_hi;
@@ -44,6 +45,7 @@ struct RowLaunch {
   RowKernel fn = nullptr;
   int threads = 0;
   bool resident = false;
+  bool persistent = false;  // grid = resident workgroups on the device, rows looped over
 };
 
 RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force);

@@ -31,10 +31,10 @@ __device__ __forceinline__ TokenOut token_math(const RowArgs& a, int64_t row, fl
   const float lse = lse2 * kLn2;
   const float lp = zy - lse;
   o.lp = lp;
-  const float lp_ref = a.lp_ref[row];
-  const float lp_mu = a.lp_mu[row];
-  const float A = a.adv[row];
-  const float ts = a.tscale ? a.tscale[row] : 1.0f;
+  const float lp_ref = uload(a.lp_ref + row);
+  const float lp_mu = uload(a.lp_mu + row);
+  const float A = uload(a.adv + row);
+  const float ts = a.tscale ? uload(a.tscale + row) : 1.0f;
   // Eq. 1 / Sec. 3.2: r_s = pi_theta / pi_ref, r_d = pi_ref / mu_old.
   const float r_s = expf(lp - lp_ref);
   const float r_d = expf(lp_ref - lp_mu);
@@ -62,7 +62,8 @@ __device__ __forceinline__ TokenOut token_math(const RowArgs& a, int64_t row, fl
 
 __device__ __forceinline__ float row_scale(const RowArgs& a) {
   if (a.scale_mode == DPPO_SCALE_TOKEN_MEAN) {
-    const int n = a.stats[DPPO_STAT_N_VALID];
+    // written by the count kernel before this one; constant while this kernel runs
+    const int n = uload(a.stats + DPPO_STAT_N_VALID);
     return a.loss_scale / (float)(n > 1 ? n : 1);
   }
   return a.loss_scale;
@@ -128,6 +129,7 @@ __device__ __forceinline__ float row_factor(float w, float n_mine, float lse2) {
 // backward constants (w, lse2, dy) in LDS. Returns through `bc`.
 struct Bcast {
   float w, lse2, dy;
+  float zy;  // z[y], published by the thread that holds it
 };
 
 __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float zy,
@@ -152,154 +154,186 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 }
 
 // ---------------------------------------------------------------------------------------
-// Register-resident row kernel, bf16 logits. NT threads x NC 16-byte chunks per thread;
-// thread tid owns chunks c * NT + tid. All row traffic goes through raw buffer accesses:
-// one VGPR offset per thread, the chunk offset c * NT * 16 in an SGPR.
+// Register-resident row kernel, bf16 logits: persistent, one workgroup per CU slot.
+//
+// NT threads x NC 16-byte chunks hold a whole row; thread tid owns chunks c * NT + tid.
+// All row traffic uses raw buffer accesses (one VGPR offset per thread, the chunk offset
+// c * NT * 16 in an SGPR, range-checked against the row). Per row:
+//   pass A  chunks are consumed in arrival order; chunk c gets an integer log2 shift
+//           n_c = ceil(L * max(chunk)), its elements become 2^(zL - n_c) in (0, 1], are
+//           summed and stored back in place as fp16 pairs; (n_c, sum) merges into (N, S);
+//   merge   workgroup merge of (N, S) -> lse2; thread 0 does the token math;
+//   pass B  dlogits chunk c = w * 2^(n_c - lse2) * e (v_fma_mix), bf16-packed and stored
+//           non-temporally; the freed registers of chunk c immediately receive chunk c of
+//           the workgroup's next row, so the next row's loads overlap this row's stores.
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD>
 __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
-  const int64_t row = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int V = a.V;
-  const int nfull = V >> 3;                 // 16-byte chunks fully inside the row
+  // Per-chunk shifts n_c live in LDS (NC x NT floats, conflict-free [c][tid] layout): the
+  // registers are reserved for the row itself.
+  __shared__ float nch[BWD ? NC : 1][NT];
   const bool loss_mode = a.mode != kModeLogprob;
-  const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
-  const int64_t y = a.ids[row];
-  const bool good = (y >= 0) && (y < V);
-  if (loss_mode && !(valid && good)) {
-    skip_row_resident<NT, NC, 2>(a, row, valid);
-    return;
-  }
-  const uint16_t* zrow = (const uint16_t*)a.logits + row * a.ld;
-  float zy = 0.0f;
-  if (tid == 0 && good) zy = bf16_to_f32(zrow[y]);
+  const bool want_d = BWD && a.dlogits != nullptr;
 
-  const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, V * 2);
-  const int voff = tid * 16;
+  // A row is read unless it is a masked or bad-id row of the loss.
+  auto reads = [&](int64_t rr) -> bool {
+    if (!loss_mode) return true;
+    if (a.mask != nullptr && uload(a.mask + rr) == 0) return false;
+    const int64_t yy = uload(a.ids + rr);
+    return yy >= 0 && yy < a.V;
+  };
+  // Every load and store of the row goes through a buffer resource; a resource with
+  // num_records = 0 turns an access into a no-op (loads read zeros, stores are dropped),
+  // which keeps the chunk loops free of branches.
   uint32_t r[NC][4];
+  int64_t row = blockIdx.x;
+  bool rd_cur = row < a.T && reads(row);
+  {
+    const __amdgpu_buffer_rsrc_t rz =
+        row_rsrc((const uint16_t*)a.logits + (rd_cur ? row : 0) * a.ld, rd_cur ? a.V * 2 : 0);
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const u32x4 v = buf_load16(rz, voff, c * NT * 16);
-    r[c][0] = v.x; r[c][1] = v.y; r[c][2] = v.z; r[c][3] = v.w;
+    for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
   }
-  // Slots that can run past the last full chunk: pad with -inf (uniform test per slot).
+  for (; row < a.T; row += gridDim.x) {
+    const int tid = threadIdx.x;
+    const int V = a.V;
+    const int voff = tid * 16;
+    const int nfull = V >> 3;               // 16-byte chunks of a row (V % 8 == 0 here)
+    // Slots c < cb are inside the row for every thread, slot cb only for threads with
+    // lane_in, slots above cb for none. Chunks outside the row read as zeros (buffer
+    // range check) and are dropped from the sums and from the stores.
+    const int cb = nfull / NT;
+    const bool lane_in = tid < nfull - cb * NT;
+
+    const int64_t next = row + gridDim.x;
+    const bool rd_next = next < a.T && reads(next);
+    const int64_t y = uload(a.ids + row);
+    const bool good = (y >= 0) && (y < V);
+    float w = 0.0f, dy = 0.0f, l2 = 0.0f;
+
+    if (rd_cur) {
+      // z[y] through the scalar unit (the aligned 32-bit word holding it). The row's bytes
+      // are written, in place, only by this workgroup and only after this read.
+      float zy = 0.0f;
+      if (good) {
+        const uint64_t off = (uint64_t)(row * a.ld + y) * 2u;
+        const uint32_t wv = uload((const uint32_t*)((const char*)a.logits + (off & ~(uint64_t)3)));
+        zy = (off & 2u) ? bf16_hi(wv) : bf16_lo(wv);
+      }
+      // Pass A.
+      float N = -INFINITY, S = 0.0f;
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    if ((c + 1) * NT > nfull && c * NT + tid >= nfull) {
-      r[c][0] = r[c][1] = r[c][2] = r[c][3] = kBf16NegInfPair;
+      for (int c = 0; c < NC; ++c) {
+        float x[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          x[2 * k] = bf16_lo(r[c][k]);
+          x[2 * k + 1] = bf16_hi(r[c][k]);
+        }
+        const float cm = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
+        float nc = __builtin_ceilf(cm * kLog2e);
+        const float sh = (nc == -INFINITY) ? 0.0f : nc;
+        float e[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) e[j] = exp2_hw(__builtin_fmaf(x[j], kLog2e, -sh));
+        float sc = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+        // a chunk outside the row contributes nothing
+        const bool dead = (c > cb) || (c == cb && !lane_in);
+        nc = dead ? -INFINITY : nc;
+        sc = dead ? 0.0f : sc;
+        if (BWD) {
+          // Pack here: left to itself the compiler sinks the packing to pass B and keeps
+          // the fp32 exponentials of every chunk alive across the merge.
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            r[c][k] = pack_f16(e[2 * k], e[2 * k + 1]);
+            asm volatile("" : "+v"(r[c][k]));
+          }
+          nch[c][tid] = nc;
+        }
+        const float Nn = fmaxf(N, nc);
+        S = S * ((N == Nn) ? 1.0f : exp2_hw(N - Nn)) + sc * ((nc == Nn) ? 1.0f : exp2_hw(nc - Nn));
+        N = Nn;
+        // Keep chunk order: the loads were issued in the previous iteration, so the
+        // scheduler would otherwise unpack every chunk at once.
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      float n = N;
+      float s = S;
+      block_merge_ns<NT>(n, s, red);
+      // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
+      const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+      finish_row(a, row, zy, lse2, good, &bc);
+      if (want_d) {
+        __syncthreads();
+        w = bc.w;
+        dy = bc.dy;
+        l2 = bc.lse2;
+      }
+    } else {                                // masked row, or a bad id on a valid row
+      // Redefine the registers on this path too, so that both paths leave a fresh value
+      // (otherwise the allocator keeps the row and its exponentials apart).
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) r[c][k] = 0u;
     }
-  }
-  // Ragged tail (V % 8 != 0): the chunk's owner reloads its elements one by one.
-  const int tail_slot = nfull / NT;
-  const bool tail_owner = (V & 7) != 0 && tid == nfull % NT;
-  if (tail_owner) {
+    if (!rd_cur && tid == 0) {
+      const bool valid = a.mask == nullptr || uload(a.mask + row) != 0;
+      a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
+      a.loss_tok[row] = 0.0f;
+      if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
+      if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+    }
+
+    // Pass B: dlogits of this row, and the only place the registers are refilled: chunk c
+    // of the next row as soon as chunk c of this row has been consumed. For a row that was
+    // not read the dlogits stores are dropped and zeros are written after the loop.
+    uint16_t* drow = want_d ? (uint16_t*)a.dlogits + row * a.ldd : nullptr;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, (want_d && rd_cur) ? V * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rn = row_rsrc(
+        (const uint16_t*)a.logits + (rd_next ? next : row) * a.ld, rd_next ? V * 2 : 0);
+    const float wf = rd_cur ? w : 0.0f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      if (c == tail_slot) {
+      if (BWD) {
+        // softmax(z)[v] = e_v * 2^(n_c - lse2); a chunk of -inf holds zeros; a NaN lse
+        // (non-finite row) makes every element NaN, as 0 * NaN does.
+        const float ncv = nch[c][tid];
+        const float f = (l2 != l2) ? l2 : ((ncv == -INFINITY) ? 0.0f : wf * exp2_hw(ncv - l2));
+        float o[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int e = nfull * 8 + j;
-          if (e < V) {
-            const uint32_t h = zrow[e];
-            const int k = j >> 1;
-            r[c][k] = (j & 1) ? ((r[c][k] & 0x0000FFFFu) | (h << 16)) : ((r[c][k] & 0xFFFF0000u) | h);
-          }
+        for (int k = 0; k < 4; ++k) {
+          o[2 * k] = f16_lo_mul(r[c][k], f);
+          o[2 * k + 1] = f16_hi_mul(r[c][k], f);
         }
+        load16(r[c], rn, voff, c * NT * 16);   // chunk c's registers are free again
+        // stores past the row fall outside the buffer range and are dropped
+        u32x4 v;
+        v.x = pack_bf16(o[0], o[1]);
+        v.y = pack_bf16(o[2], o[3]);
+        v.z = pack_bf16(o[4], o[5]);
+        v.w = pack_bf16(o[6], o[7]);
+        buf_store16_nt(v, rd, voff, c * NT * 16);
+      } else {
+        load16(r[c], rn, voff, c * NT * 16);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
-  }
-
-  // Pass 1: the thread's maximum.
-  float m = -INFINITY;
+    if (want_d && !rd_cur) {                // zeros for a row that was not read
+      const __amdgpu_buffer_rsrc_t rz = row_rsrc(drow, V * 2);
+      const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) m = max3(m, bf16_lo(r[c][k]), bf16_hi(r[c][k]));
-
-  // Keep the packed words as the only live copy of the row: without this barrier the
-  // compiler reuses the unpacked floats of pass 1 in pass 2 and spills them.
-#pragma unroll
-  for (int c = 0; c < NC; ++c)
-#pragma unroll
-    for (int k = 0; k < 4; ++k) asm volatile("" : "+v"(r[c][k]));
-
-  // Pass 2: sum of 2^(zL - n); the exponentials replace the logits as fp16 pairs.
-  const float n_shift = (m == -INFINITY) ? 0.0f : m * kLog2e;
-  const float nb = -n_shift;
-  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    float e[8];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      e[2 * k] = exp2_hw(__builtin_fmaf(bf16_lo(r[c][k]), kLog2e, nb));
-      e[2 * k + 1] = exp2_hw(__builtin_fmaf(bf16_hi(r[c][k]), kLog2e, nb));
+      for (int c = 0; c < NC; ++c) buf_store16_nt(zero, rz, voff, c * NT * 16);
     }
-    s0 += e[0] + e[1];
-    s1 += e[2] + e[3];
-    s2 += e[4] + e[5];
-    s3 += e[6] + e[7];
-    if (BWD) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) r[c][k] = pack_f16(e[2 * k], e[2 * k + 1]);
-    }
-  }
-  if (BWD) {
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) asm volatile("" : "+v"(r[c][k]));
-  }
-  float n = (m == -INFINITY) ? -INFINITY : n_shift;
-  float s = (s0 + s1) + (s2 + s3);
-  const float n_mine = n;
-  block_merge_ns<NT>(n, s, red);
-  // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
-  const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
-
-  finish_row(a, row, zy, lse2, good, &bc);
-  if (!BWD || !a.dlogits) return;
-  __syncthreads();
-  const float w = bc.w;
-  const float dy = bc.dy;
-  // softmax(z)[v] = e_v * 2^(n_mine - lse2). A thread whose elements are all -inf holds
-  // zeros; a NaN lse (non-finite row) makes every element NaN, as 0 * NaN does.
-  const float f = row_factor(w, n_mine, bc.lse2);
-
-  uint16_t* drow = (uint16_t*)a.dlogits + row * a.ldd;
-  const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, V * 2);
-  const int cy = (int)(y >> 3);
-  const int my_slot = (cy % NT == tid) ? cy / NT : -1;
-  const int jy = (int)(y & 7);
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int idx = c * NT + tid;
-    float o[8];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      o[2 * k] = f16_lo_mul(r[c][k], f);
-      o[2 * k + 1] = f16_hi_mul(r[c][k], f);
-    }
-    if (c == my_slot) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) o[j] = (j == jy) ? dy : o[j];
-    }
-    if ((c + 1) * NT <= nfull || idx < nfull) {
-      u32x4 v;
-      v.x = pack_bf16(o[0], o[1]);
-      v.y = pack_bf16(o[2], o[3]);
-      v.z = pack_bf16(o[4], o[5]);
-      v.w = pack_bf16(o[6], o[7]);
-      buf_store16_nt(v, rd, voff, c * NT * 16);
-    } else if (tail_owner && c == tail_slot) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int e = nfull * 8 + j;
-        if (e < V) drow[e] = to_bf16(o[j]);
-      }
-    }
+    // dlogits at v = y is w (p_y - 1) = w expm1(lp), computed once by thread 0. The thread
+    // whose chunk holds y writes it over its own vector store above: two stores of one
+    // thread to one address, through the same buffer path, land in program order.
+    if (want_d && rd_cur && good && tid == (int)((y >> 3) % NT))
+      __builtin_amdgcn_raw_buffer_store_b16(to_bf16(dy), rd, (int)(y * 2), 0, kAuxNT);
+    rd_cur = rd_next;
   }
 }
 
@@ -610,8 +644,8 @@ struct ResCfg {
   int nt, nc;
 };
 // Resident shapes, by capacity in 16-byte chunks (NT * NC).
-constexpr ResCfg kResident[] = {{256, 1},  {256, 2},  {256, 4},   {512, 4},   {512, 6},  {512, 8},
-                                {1024, 6}, {1024, 8}, {1024, 12}, {1024, 16}, {1024, 19}};
+constexpr ResCfg kResident[] = {{256, 1},  {256, 2},  {256, 4},  {512, 4},  {512, 6},
+                                {512, 8},  {512, 12}, {512, 16}, {512, 24}, {512, 38}};
 constexpr int kNumResident = sizeof(kResident) / sizeof(kResident[0]);
 
 template <bool BWD>
@@ -623,11 +657,10 @@ RowKernel pick_bf16(int i) {
     case 3: return rows_bf16_resident<512, 4, BWD>;
     case 4: return rows_bf16_resident<512, 6, BWD>;
     case 5: return rows_bf16_resident<512, 8, BWD>;
-    case 6: return rows_bf16_resident<1024, 6, BWD>;
-    case 7: return rows_bf16_resident<1024, 8, BWD>;
-    case 8: return rows_bf16_resident<1024, 12, BWD>;
-    case 9: return rows_bf16_resident<1024, 16, BWD>;
-    default: return rows_bf16_resident<1024, 19, BWD>;
+    case 6: return rows_bf16_resident<512, 12, BWD>;
+    case 7: return rows_bf16_resident<512, 16, BWD>;
+    case 8: return rows_bf16_resident<512, 24, BWD>;
+    default: return rows_bf16_resident<512, 38, BWD>;
   }
 }
 template <bool BWD>
@@ -639,11 +672,10 @@ RowKernel pick_f32(int i) {
     case 3: return rows_f32_resident<512, 4, BWD>;
     case 4: return rows_f32_resident<512, 6, BWD>;
     case 5: return rows_f32_resident<512, 8, BWD>;
-    case 6: return rows_f32_resident<1024, 6, BWD>;
-    case 7: return rows_f32_resident<1024, 8, BWD>;
-    case 8: return rows_f32_resident<1024, 12, BWD>;
-    case 9: return rows_f32_resident<1024, 16, BWD>;
-    default: return rows_f32_resident<1024, 19, BWD>;
+    case 6: return rows_f32_resident<512, 12, BWD>;
+    case 7: return rows_f32_resident<512, 16, BWD>;
+    case 8: return rows_f32_resident<512, 24, BWD>;
+    default: return rows_f32_resident<512, 38, BWD>;
   }
 }
 }  // namespace
@@ -653,7 +685,8 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   const int esize = dtype == DPPO_BF16 ? 2 : 4;
   const int64_t chunks = (V * esize + 15) / 16;
   int pick = -1;
-  if (aligned && force != kForceStream) {
+  const bool whole_chunks = (V * esize) % 16 == 0;
+  if (aligned && whole_chunks && force != kForceStream) {
     for (int i = 0; i < kNumResident; ++i) {
       if ((int64_t)kResident[i].nt * kResident[i].nc >= chunks) {
         pick = i;
@@ -666,6 +699,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
     L.fn = dtype == DPPO_BF16 ? (bwd ? pick_bf16<true>(pick) : pick_bf16<false>(pick))
                               : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
     L.resident = true;
+    L.persistent = dtype == DPPO_BF16;
     return L;
   }
   L.threads = 1024;
