@@ -67,6 +67,8 @@ __device__ __forceinline__ float f16_hi_mul(uint32_t u, float f) {
 }
 
 // Merge two log2-domain partials (n, s) into (n, s). A partial with n = -inf is empty.
+// Symmetric: merge(a, b) and merge(b, a) give the same bits, so every lane of a butterfly
+// ends with the same result.
 __device__ __forceinline__ void merge_ns(float& n, float& s, float n2, float s2) {
   const float N = fmaxf(n, n2);
   const float fa = (n == N) ? 1.0f : exp2f(n - N);
@@ -75,8 +77,101 @@ __device__ __forceinline__ void merge_ns(float& n, float& s, float n2, float s2)
   n = N;
 }
 
-// Workgroup-wide merge of (n, s); every thread returns the row result. `lds` holds
-// 2 * (NT / 64) + 2 floats. Fixed reduction order: the result is reproducible.
+// The same merge for integer-valued shifts, where 2^(n - N) is exact on v_exp_f32.
+__device__ __forceinline__ void merge_ns_int(float& n, float& s, float n2, float s2) {
+  const float N = fmaxf(n, n2);
+  const float fa = (n == N) ? 1.0f : exp2_hw(n - N);
+  const float fb = (n2 == N) ? 1.0f : exp2_hw(n2 - N);
+  s = s * fa + s2 * fb;
+  n = N;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               0xF, 0xF, false));
+}
+
+// Wave-wide merge of integer-shift partials; every lane returns the wave's result.
+// Quad xor 1 and xor 2, half-row and row mirrors (DPP) reduce each 16-lane row; the
+// permlane swaps combine rows 0-1, 2-3 and then the two halves.
+__device__ __forceinline__ void wave_merge_ns_int(float& n, float& s) {
+  merge_ns_int(n, s, dpp_f<0xB1>(n), dpp_f<0xB1>(s));    // quad_perm [1,0,3,2]
+  merge_ns_int(n, s, dpp_f<0x4E>(n), dpp_f<0x4E>(s));    // quad_perm [2,3,0,1]
+  merge_ns_int(n, s, dpp_f<0x141>(n), dpp_f<0x141>(s));  // row_half_mirror
+  merge_ns_int(n, s, dpp_f<0x140>(n), dpp_f<0x140>(s));  // row_mirror
+  {
+    const auto pn = __builtin_amdgcn_permlane16_swap(__float_as_uint(n), __float_as_uint(n), false, false);
+    const auto ps = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+    n = __uint_as_float(pn[0]);
+    s = __uint_as_float(ps[0]);
+    merge_ns_int(n, s, __uint_as_float(pn[1]), __uint_as_float(ps[1]));
+  }
+  {
+    const auto pn = __builtin_amdgcn_permlane32_swap(__float_as_uint(n), __float_as_uint(n), false, false);
+    const auto ps = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+    n = __uint_as_float(pn[0]);
+    s = __uint_as_float(ps[0]);
+    merge_ns_int(n, s, __uint_as_float(pn[1]), __uint_as_float(ps[1]));
+  }
+}
+
+// Workgroup-wide merge of integer-shift partials with a single barrier. `lds` holds
+// 2 * (NT / 64) floats and must not be reused by the workgroup before its next barrier
+// (callers alternate two buffers). Every thread returns the same bits: each wave merges
+// the NT / 64 wave results in the same fixed tree.
+template <int NT>
+__device__ __forceinline__ void block_merge_ns_int(float& n, float& s, float* lds) {
+  constexpr int NW = NT / 64;
+  static_assert(NW <= 16, "one 16-lane row merges the wave results");
+  wave_merge_ns_int(n, s);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    lds[wave] = n;
+    lds[NW + wave] = s;
+  }
+  __syncthreads();
+  const int l = threadIdx.x & 15;
+  n = l < NW ? lds[l] : -INFINITY;
+  s = l < NW ? lds[NW + l] : 0.0f;
+  merge_ns_int(n, s, dpp_f<0xB1>(n), dpp_f<0xB1>(s));
+  merge_ns_int(n, s, dpp_f<0x4E>(n), dpp_f<0x4E>(s));
+  merge_ns_int(n, s, dpp_f<0x141>(n), dpp_f<0x141>(s));
+  merge_ns_int(n, s, dpp_f<0x140>(n), dpp_f<0x140>(s));
+}
+
+// Raw buffer resources (gfx9-family descriptor: stride 0, 32-bit data format). Loads past
+// num_records return zeros and stores past it are dropped, so a row's resource bounds
+// every access to that row.
+constexpr int kRsrcFlags = 0x00020000;
+constexpr int kAuxNT = 2;  // non-temporal cache policy bit for buffer accesses on gfx950
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, kRsrcFlags);
+}
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+__device__ __forceinline__ void load16(uint32_t (&d)[4], __amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  d[0] = v.x;
+  d[1] = v.y;
+  d[2] = v.z;
+  d[3] = v.w;
+}
+__device__ __forceinline__ void buf_store16_nt(u32x4 v, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
+}
+
+// Load of a value at a workgroup-uniform address through the scalar unit (constant
+// address space): waited on with lgkmcnt, so it never waits behind the row's vector loads.
+template <typename T>
+__device__ __forceinline__ T uload(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
+}
+
+// Workgroup-wide merge of general (n, s) partials (two barriers, shuffles). Fixed
+// reduction order: the result is reproducible.
 template <int NT>
 __device__ __forceinline__ void block_merge_ns(float& n, float& s, float* lds) {
   constexpr int NW = NT / 64;
@@ -112,36 +207,6 @@ __device__ __forceinline__ void block_merge_ns(float& n, float& s, float* lds) {
     n = lds[2 * NW];
     s = lds[2 * NW + 1];
   }
-}
-
-// Raw buffer resources (gfx9-family descriptor: stride 0, 32-bit data format). Loads past
-// num_records return zeros and stores past it are dropped, so a row's resource bounds
-// every access to that row.
-constexpr int kRsrcFlags = 0x00020000;
-constexpr int kAuxNT = 2;  // non-temporal cache policy bit for buffer accesses on gfx950
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, kRsrcFlags);
-}
-__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
-}
-__device__ __forceinline__ void load16(uint32_t (&d)[4], __amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
-  d[0] = v.x;
-  d[1] = v.y;
-  d[2] = v.z;
-  d[3] = v.w;
-}
-__device__ __forceinline__ void buf_store16_nt(u32x4 v, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
-}
-
-// Load of a value at a workgroup-uniform address through the scalar unit (constant
-// address space): waited on with lgkmcnt, so it never waits behind the row's vector loads.
-template <typename T>
-__device__ __forceinline__ T uload(const T* p) {
-  return *(const __attribute__((address_space(4))) T*)p;
 }
 
 // numpy-style minimum: NaN if either operand is NaN.

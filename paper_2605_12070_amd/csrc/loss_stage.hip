@@ -25,16 +25,39 @@ struct TokenOut {
   uint8_t flags;
 };
 
-__device__ __forceinline__ TokenOut token_math(const RowArgs& a, int64_t row, float zy,
-                                               float lse2, float scale) {
+// Per-token inputs of a row, read through the scalar unit.
+struct TokenIn {
+  float lp_ref, lp_mu, adv, ts, scale;
+};
+
+__device__ __forceinline__ float row_scale(const RowArgs& a);
+
+__device__ __forceinline__ TokenIn token_inputs(const RowArgs& a, int64_t row) {
+  TokenIn t;
+  if (a.mode == kModeLogprob) {
+    t.lp_ref = t.lp_mu = t.adv = 0.0f;
+    t.ts = t.scale = 1.0f;
+    return t;
+  }
+  t.lp_ref = uload(a.lp_ref + row);
+  t.lp_mu = uload(a.lp_mu + row);
+  t.adv = uload(a.adv + row);
+  t.ts = a.tscale ? uload(a.tscale + row) : 1.0f;
+  t.scale = row_scale(a);
+  return t;
+}
+
+__device__ __forceinline__ TokenOut token_math(const RowArgs& a, const TokenIn& t, float zy,
+                                               float lse2) {
   TokenOut o;
   const float lse = lse2 * kLn2;
   const float lp = zy - lse;
   o.lp = lp;
-  const float lp_ref = uload(a.lp_ref + row);
-  const float lp_mu = uload(a.lp_mu + row);
-  const float A = uload(a.adv + row);
-  const float ts = a.tscale ? uload(a.tscale + row) : 1.0f;
+  const float lp_ref = t.lp_ref;
+  const float lp_mu = t.lp_mu;
+  const float A = t.adv;
+  const float ts = t.ts;
+  const float scale = t.scale;
   // Eq. 1 / Sec. 3.2: r_s = pi_theta / pi_ref, r_d = pi_ref / mu_old.
   const float r_s = expf(lp - lp_ref);
   const float r_d = expf(lp_ref - lp_mu);
@@ -133,7 +156,7 @@ struct Bcast {
 };
 
 __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float zy,
-                                           float lse2, bool good, Bcast* bc) {
+                                           float lse2, bool good, Bcast* bc, const TokenIn& tin) {
   if (a.mode == kModeLogprob) {
     if (threadIdx.x == 0) {
       a.lp_out[row] = good ? zy - lse2 * kLn2 : __builtin_nanf("");
@@ -142,7 +165,7 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
     return;
   }
   if (threadIdx.x == 0) {
-    const TokenOut o = token_math(a, row, zy, lse2, row_scale(a));
+    const TokenOut o = token_math(a, tin, zy, lse2);
     a.lp_out[row] = o.lp;
     a.loss_tok[row] = o.loss;
     if (a.flags) a.flags[row] = o.flags;
@@ -169,7 +192,7 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD>
 __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
-  __shared__ float red[2 * (NT / 64) + 2];
+  __shared__ float red[2][2 * (NT / 64)];   // alternated by row parity: one barrier per merge
   __shared__ Bcast bc;
   // Per-chunk shifts n_c live in LDS (NC x NT floats, conflict-free [c][tid] layout): the
   // registers are reserved for the row itself.
@@ -196,7 +219,8 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
   }
-  for (; row < a.T; row += gridDim.x) {
+  int parity = 0;
+  for (; row < a.T; row += gridDim.x, parity ^= 1) {
     const int tid = threadIdx.x;
     const int V = a.V;
     const int voff = tid * 16;
@@ -211,6 +235,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
     const bool rd_next = next < a.T && reads(next);
     const int64_t y = uload(a.ids + row);
     const bool good = (y >= 0) && (y < V);
+    const TokenIn tin = token_inputs(a, row);   // scalar loads, in flight during pass A
     float w = 0.0f, dy = 0.0f, l2 = 0.0f;
 
     if (rd_cur) {
@@ -253,19 +278,17 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
           }
           nch[c][tid] = nc;
         }
-        const float Nn = fmaxf(N, nc);
-        S = S * ((N == Nn) ? 1.0f : exp2_hw(N - Nn)) + sc * ((nc == Nn) ? 1.0f : exp2_hw(nc - Nn));
-        N = Nn;
+        merge_ns_int(N, S, nc, sc);
         // Keep chunk order: the loads were issued in the previous iteration, so the
         // scheduler would otherwise unpack every chunk at once.
         __builtin_amdgcn_sched_barrier(0);
       }
       float n = N;
       float s = S;
-      block_merge_ns<NT>(n, s, red);
+      block_merge_ns_int<NT>(n, s, red[parity]);
       // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
       const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
-      finish_row(a, row, zy, lse2, good, &bc);
+      finish_row(a, row, zy, lse2, good, &bc, tin);
       if (want_d) {
         __syncthreads();
         w = bc.w;
@@ -288,9 +311,9 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
       if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
     }
 
-    // Pass B: dlogits of this row, and the only place the registers are refilled: chunk c
-    // of the next row as soon as chunk c of this row has been consumed. For a row that was
-    // not read the dlogits stores are dropped and zeros are written after the loop.
+    // Pass B: dlogits of this row, then the only place the registers are refilled: the
+    // next row's chunks. For a row that was not read the dlogits stores are dropped and
+    // zeros are written below.
     uint16_t* drow = want_d ? (uint16_t*)a.dlogits + row * a.ldd : nullptr;
     const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, (want_d && rd_cur) ? V * 2 : 0);
     const __amdgpu_buffer_rsrc_t rn = row_rsrc(
@@ -309,7 +332,6 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
           o[2 * k] = f16_lo_mul(r[c][k], f);
           o[2 * k + 1] = f16_hi_mul(r[c][k], f);
         }
-        load16(r[c], rn, voff, c * NT * 16);   // chunk c's registers are free again
         // stores past the row fall outside the buffer range and are dropped
         u32x4 v;
         v.x = pack_bf16(o[0], o[1]);
@@ -317,11 +339,14 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
         v.z = pack_bf16(o[4], o[5]);
         v.w = pack_bf16(o[6], o[7]);
         buf_store16_nt(v, rd, voff, c * NT * 16);
-      } else {
-        load16(r[c], rn, voff, c * NT * 16);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    // All of this row's stores are issued before any load of the next row: the vector
+    // memory counter retires in order, and loads queued behind interleaved stores would
+    // make every wait in the next row's pass A also wait for store acknowledgements.
+#pragma unroll
+    for (int c = 0; c < NC; ++c) load16(r[c], rn, voff, c * NT * 16);
     if (want_d && !rd_cur) {                // zeros for a row that was not read
       const __amdgpu_buffer_rsrc_t rz = row_rsrc(drow, V * 2);
       const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -416,7 +441,7 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgs a) {
   block_merge_ns<NT>(n, s, red);
   const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
 
-  finish_row(a, row, zy, lse2, good, &bc);
+  finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row));
   if (!BWD || !a.dlogits) return;
   __syncthreads();
   const float w = bc.w;
@@ -561,7 +586,7 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgs a) {
   block_merge_ns<NT>(n, s, red);
   const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
 
-  finish_row(a, row, zy, lse2, good, &bc);
+  finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row));
   if (!BWD || !a.dlogits) return;
   __syncthreads();
   const float w = bc.w;
@@ -644,8 +669,8 @@ struct ResCfg {
   int nt, nc;
 };
 // Resident shapes, by capacity in 16-byte chunks (NT * NC).
-constexpr ResCfg kResident[] = {{256, 1},  {256, 2},  {256, 4},  {512, 4},  {512, 6},
-                                {512, 8},  {512, 12}, {512, 16}, {512, 24}, {512, 38}};
+constexpr ResCfg kResident[] = {{256, 1},  {256, 2},   {256, 4},   {512, 4},   {512, 6},
+                                {512, 8},  {1024, 6}, {1024, 8}, {1024, 12}, {1024, 19}};
 constexpr int kNumResident = sizeof(kResident) / sizeof(kResident[0]);
 
 template <bool BWD>
@@ -657,10 +682,10 @@ RowKernel pick_bf16(int i) {
     case 3: return rows_bf16_resident<512, 4, BWD>;
     case 4: return rows_bf16_resident<512, 6, BWD>;
     case 5: return rows_bf16_resident<512, 8, BWD>;
-    case 6: return rows_bf16_resident<512, 12, BWD>;
-    case 7: return rows_bf16_resident<512, 16, BWD>;
-    case 8: return rows_bf16_resident<512, 24, BWD>;
-    default: return rows_bf16_resident<512, 38, BWD>;
+    case 6: return rows_bf16_resident<1024, 6, BWD>;
+    case 7: return rows_bf16_resident<1024, 8, BWD>;
+    case 8: return rows_bf16_resident<1024, 12, BWD>;
+    default: return rows_bf16_resident<1024, 19, BWD>;
   }
 }
 template <bool BWD>
@@ -672,10 +697,10 @@ RowKernel pick_f32(int i) {
     case 3: return rows_f32_resident<512, 4, BWD>;
     case 4: return rows_f32_resident<512, 6, BWD>;
     case 5: return rows_f32_resident<512, 8, BWD>;
-    case 6: return rows_f32_resident<512, 12, BWD>;
-    case 7: return rows_f32_resident<512, 16, BWD>;
-    case 8: return rows_f32_resident<512, 24, BWD>;
-    default: return rows_f32_resident<512, 38, BWD>;
+    case 6: return rows_f32_resident<1024, 6, BWD>;
+    case 7: return rows_f32_resident<1024, 8, BWD>;
+    case 8: return rows_f32_resident<1024, 12, BWD>;
+    default: return rows_f32_resident<1024, 19, BWD>;
   }
 }
 }  // namespace
