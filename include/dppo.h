@@ -175,6 +175,13 @@ dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, in
  * 1 = always the streaming kernel. Process-global; any other value is INVALID_ARG. */
 dppo_status dppo_set_path_policy(int32_t policy);
 
+/* Name of the per-row kernel (as profilers print it) that a call with this logits dtype,
+ * row length V and row stride ld (elements) launches under the current path policy,
+ * assuming 16-byte-aligned base pointers; with_dlogits != 0 for the fused backward.
+ * Pure host logic, no HIP call. The string is owned by the library and valid until the
+ * next call on this host thread. NULL for an invalid dtype or V < 1 or ld < V. */
+const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t with_dlogits);
+
 /* Static description of a status code. */
 const char* dppo_strerror(dppo_status s);
 

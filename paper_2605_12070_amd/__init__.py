@@ -23,7 +23,7 @@ from ._lib import (DppoError, FLAG_BAD_ID, FLAG_BAND, FLAG_PPO, FLAG_VALID,  # n
 __all__ = [
     "logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "ewma_proxy_update", "LossResult",
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
-    "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer",
+    "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name",
 ]
 
 
@@ -151,6 +151,16 @@ def set_path_policy(policy: str):
     """'auto' (register-resident rows when they fit) or 'stream' (always two-pass)."""
     code = {"auto": 0, "stream": 1}[policy]
     _lib.check(_lib.lib().dppo_set_path_policy(code), "dppo_set_path_policy")
+
+
+def row_kernel_name(dtype: torch.dtype, V: int, ld: int | None = None,
+                    with_dlogits: bool = True) -> str:
+    """Profiler name of the per-row kernel a call with these shapes launches."""
+    code = {torch.float32: 0, torch.bfloat16: 1}[dtype]
+    name = _lib.lib().dppo_row_kernel_name(code, V, V if ld is None else ld, int(with_dlogits))
+    if name is None:
+        raise ValueError(f"no row kernel for dtype={dtype}, V={V}, ld={ld}")
+    return name.decode()
 
 
 class KernelTimer:

@@ -42,6 +42,7 @@ SIGNATURES = {
     "dppo_set_path_policy": (I32, [I32]),
     "dppo_timer_enable": (I32, [I32]),
     "dppo_timer_read": (I32, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+    "dppo_row_kernel_name": (C.c_char_p, [I32, I64, I64, I32]),
 }
 
 _lock = threading.Lock()

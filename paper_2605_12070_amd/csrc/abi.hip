@@ -185,6 +185,21 @@ dppo_status dppo_timer_read(double* total_ms, int64_t* launches) {
   return DPPO_OK;
 }
 
+const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t with_dlogits) {
+  if ((dtype != DPPO_F32 && dtype != DPPO_BF16) || V < 1 || ld < V) return nullptr;
+  const bool aligned = (ld * esize_of(dtype)) % 16 == 0;
+  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, with_dlogits != 0, g_path_policy);
+  thread_local char buf[96];
+  const char* ty = dtype == DPPO_BF16 ? "bf16" : "f32";
+  const char* bw = with_dlogits ? "true" : "false";
+  if (L.resident)
+    snprintf(buf, sizeof(buf), "dppo::rows_%s_resident<%d, %d, %s>", ty, L.threads, L.chunks, bw);
+  else
+    snprintf(buf, sizeof(buf), "dppo::rows_stream<%s, %d, %s, %s>",
+             dtype == DPPO_BF16 ? "unsigned short" : "float", L.threads, bw, aligned ? "true" : "false");
+  return buf;
+}
+
 dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                         const int64_t* token_ids, float* logp_out, float* lse_out, void* stream) {
   dppo_status s = check_matrix(logits, dtype, T, V, ld, "logits");

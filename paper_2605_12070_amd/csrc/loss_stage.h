@@ -44,6 +44,7 @@ typedef void (*RowKernel)(RowArgs);
 struct RowLaunch {
   RowKernel fn = nullptr;
   int threads = 0;
+  int chunks = 0;            // resident kernels: 16-byte chunks per thread
   bool resident = false;
   bool persistent = false;  // grid = resident workgroups on the device, rows looped over
 };

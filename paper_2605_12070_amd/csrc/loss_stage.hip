@@ -721,6 +721,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   }
   if (pick >= 0) {
     L.threads = kResident[pick].nt;
+    L.chunks = kResident[pick].nc;
     L.fn = dtype == DPPO_BF16 ? (bwd ? pick_bf16<true>(pick) : pick_bf16<false>(pick))
                               : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
     L.resident = true;

@@ -179,3 +179,23 @@ def test_host_controller_logic():
     assert P.train_infer_mask_value([10, 9, 9, 8, 0]) == 0.8
     assert P.train_infer_mask_value([0, 0, 0, 0, 0]) == 1.0
     assert abs(P.ppo_clip_ratio([10, 9, 7, 6, 0]) - 0.3) < 1e-12
+
+
+def test_row_kernel_name_follows_the_selection_rule():
+    """Host-only query: the resident kernel while a row fits NT x NC 16-byte chunks (at most
+    1024 x 19 x 8 = 155648 bf16 elements) with whole chunks, the streaming kernel beyond."""
+    import torch
+    from paper_2605_12070_amd import row_kernel_name
+    bf, f32 = torch.bfloat16, torch.float32
+    assert row_kernel_name(bf, 151936) == "dppo::rows_bf16_resident<1024, 19, true>"
+    assert row_kernel_name(bf, 155648) == "dppo::rows_bf16_resident<1024, 19, true>"
+    assert row_kernel_name(bf, 155656).startswith("dppo::rows_stream<unsigned short, 1024, true")
+    assert row_kernel_name(bf, 151936, with_dlogits=False).endswith("<1024, 19, false>")
+    assert row_kernel_name(bf, 2048) == "dppo::rows_bf16_resident<256, 1, true>"
+    assert row_kernel_name(bf, 77825).startswith("dppo::rows_stream")      # ragged chunk
+    assert row_kernel_name(bf, 64, ld=68).endswith("true, false>")          # unaligned stride
+    assert row_kernel_name(f32, 32000) == "dppo::rows_f32_resident<1024, 8, true>"
+    L = _lib.lib()
+    assert L.dppo_row_kernel_name(7, 100, 100, 1) is None
+    assert L.dppo_row_kernel_name(1, 0, 0, 1) is None
+    assert L.dppo_row_kernel_name(1, 100, 99, 1) is None
