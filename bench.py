@@ -16,6 +16,7 @@ import hashlib
 import json
 import os
 import platform
+import re
 import sys
 import time
 
@@ -42,12 +43,13 @@ KERNEL_SOURCES = ("dppo_device.h", "loss_stage.h", "loss_stage.hip")
 
 
 def kernel_source_hash() -> str:
-    """Hash of the row kernel's device sources: a stored HBM-traffic figure is reported only
-    while it still describes the kernel being timed."""
+    """Hash of the row kernel's device sources, comments and spacing aside: a stored
+    HBM-traffic figure is reported only while it still describes the kernel being timed."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(name.encode() + f.read())
+        with open(os.path.join(CSRC, name)) as f:
+            code = re.sub(r"/\*.*?\*/|//[^\n]*", "", f.read(), flags=re.S)   # comments
+        h.update(name.encode() + " ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -187,8 +187,11 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 //           summed and stored back in place as fp16 pairs; (n_c, sum) merges into (N, S);
 //   merge   workgroup merge of (N, S) -> lse2; thread 0 does the token math;
 //   pass B  dlogits chunk c = w * 2^(n_c - lse2) * e (v_fma_mix), bf16-packed and stored
-//           non-temporally; the freed registers of chunk c immediately receive chunk c of
-//           the workgroup's next row, so the next row's loads overlap this row's stores.
+//           non-temporally; once every store of the row is issued, the registers receive
+//           the workgroup's next row (all loads issued back to back), so those loads are in
+//           flight while this row's stores drain. Stores go first because the vector
+//           memory counter retires in order: a load queued behind a store would make the
+//           next row's first wait also wait for that store.
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD>
 __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
