@@ -170,6 +170,15 @@ __device__ __forceinline__ T uload(const T* p) {
   return *(const __attribute__((address_space(4))) T*)p;
 }
 
+// A uniform byte through the scalar unit, which has no byte loads: the aligned 32-bit word
+// holding the byte (same page, so always mapped) is loaded and shifted. A plain byte load
+// would become a vector load.
+__device__ __forceinline__ uint32_t uload_u8(const uint8_t* p) {
+  const uintptr_t a = (uintptr_t)p;
+  const uint32_t w = uload((const uint32_t*)(a & ~(uintptr_t)3));
+  return (w >> ((uint32_t)(a & 3u) * 8u)) & 0xffu;
+}
+
 // Workgroup-wide merge of general (n, s) partials (two barriers, shuffles). Fixed
 // reduction order: the result is reproducible.
 template <int NT>
