@@ -121,6 +121,30 @@ def copy_bandwidth(dev, nbytes=2 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+def ewma_bandwidth(dev, n, reps=20):
+    """PPO-EWMA update of a parameter-sized fp32 buffer (normalised form: x_prox and x_new
+    are read, x_prox written, 12 bytes per element), timed with events on the stream the
+    library launches on (torch's current stream)."""
+    x_prox = torch.zeros(n, dtype=torch.float32, device=dev)
+    x_new = torch.ones(n, dtype=torch.float32, device=dev)
+    w = P.ewma_proxy_update(x_prox, x_new, 0.75, w=0.0)      # first step (copy)
+    w = P.ewma_proxy_update(x_prox, x_new, 0.75, w=w)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        w = P.ewma_proxy_update(x_prox, x_new, 0.75, w=w)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del x_prox, x_new
+    gbps = 12 * n / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(gbps / HBM_PEAK_GBPS, 4), "kernel": "dppo::ewma_kernel<false, true>",
+            "n": n, "dtype": "f32", "alg_bytes_per_launch": 12 * n, "kernel_ms": round(ms, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -130,6 +154,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy", action="store_true")
+    ap.add_argument("--ewma-elems", type=int, default=1 << 30,
+                    help="size of the parameter-sized EWMA measurement (0 to skip)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -218,6 +244,8 @@ def main():
         "hbm_pct_of_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "roofline": roofline,
     }
+    if args.ewma_elems > 0:
+        result["ewma_roofline"] = ewma_bandwidth(dev, args.ewma_elems)
     if not args.no_copy:
         result["context"] = {"d2d_copy_GBps": round(copy_bandwidth(dev), 1)}
     if not args.no_cpu_baseline:

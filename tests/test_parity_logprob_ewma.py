@@ -111,6 +111,25 @@ def test_ewma_fixed_and_unaligned(dtype):
         device=DEV).manual_seed(1), device=DEV).to(dtype)[:1]).tolist()
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("n", [1, 7, 9, 4099, 65536 * 8 + 5])
+def test_ewma_leaves_the_rest_of_the_allocation_alone(dtype, n):
+    """Vector threads and tail threads write exactly [0, n): guards after the end keep
+    their bits (the buffers are slices of larger allocations with 16-byte-aligned bases)."""
+    _say("ewma guards", dtype, n)
+    g = torch.Generator(device=DEV).manual_seed(7)
+    xb = torch.randn(n + 40, generator=g, device=DEV).to(dtype)
+    nb = torch.randn(n + 40, generator=g, device=DEV).to(dtype)
+    before = bits_of(xb)
+    P.ewma_proxy_update(xb[:n], nb[:n], 0.5, w=1.0)
+    torch.cuda.synchronize()
+    after = bits_of(xb)
+    assert np.array_equal(after[n:], before[n:])
+    ref, _ = oracle.ewma_normalized_step(before[:n], bits_of(nb[:n]), 0.5, 1.0)
+    tol = 2.0 ** -8 if dtype == torch.bfloat16 else 2e-6
+    np.testing.assert_allclose(after[:n], ref, rtol=tol, atol=tol)
+
+
 def test_ewma_controller_resets_on_low_rho():
     n = 64
     x0 = torch.zeros(n, device=DEV)
