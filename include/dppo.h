@@ -79,6 +79,17 @@ typedef enum { DPPO_SCALE_CONST = 0, DPPO_SCALE_TOKEN_MEAN = 1 } dppo_scale_mode
 #define DPPO_STAT_N_BAD 4    /* valid rows with an out-of-range token id                   */
 #define DPPO_N_STATS 5
 
+/* Where pi_ref, the policy between mu_old and pi_theta that splits the ratio, comes from.
+ *  GIVEN:      logp_ref is an input (exact old log-probs, Sec. 5.1, or the PPO-EWMA proxy,
+ *              Sec. 5.2).
+ *  LOGLINEAR:  token-wise log-linear interpolation (App. A):
+ *                log pi_ref = alpha log mu_old + (1 - alpha) log pi_theta.
+ *  LINEAR:     arithmetic interpolation (App. A): pi_ref = alpha mu_old + (1 - alpha) pi_theta.
+ * alpha in (0, 1) is the behaviour-policy weight (1 / (n + 1) for version gap n, Table 4).
+ * An interpolated pi_ref is evaluated on the current log-prob and, like any reference, is a
+ * constant with respect to theta. logp_ref is not read (may be NULL) unless GIVEN.         */
+typedef enum { DPPO_REF_GIVEN = 0, DPPO_REF_LOGLINEAR = 1, DPPO_REF_LINEAR = 2 } dppo_ref_mode;
+
 /* Knobs of the decoupled MIS objective (Eq. 2, Eq. 3, Eq. 4; Table 1).
  *  band_lo, band_hi:         r_d is kept iff band_lo <= r_d <= band_hi (inclusive, as in
  *                            Eq. 4: M_[1/c, c] is band_lo = 1/c, band_hi = c; App. A's
@@ -87,13 +98,16 @@ typedef enum { DPPO_SCALE_CONST = 0, DPPO_SCALE_TOKEN_MEAN = 1 } dppo_scale_mode
  *  clip_eps_lo, clip_eps_hi: PPO interval [1 - eps_lo, 1 + eps_hi] on r_s (Eq. 2; the
  *                            asymmetric form of App. A). Both >= 0, finite.
  *  rd_mode:                  a dppo_rd_mode.
- *  scale_mode, loss_scale:   a dppo_scale_mode and a finite multiplier.            */
+ *  scale_mode, loss_scale:   a dppo_scale_mode and a finite multiplier.
+ *  ref_mode, alpha:          a dppo_ref_mode; alpha in (0, 1) unless ref_mode is GIVEN. */
 typedef struct dppo_params {
   float band_lo, band_hi;
   float clip_eps_lo, clip_eps_hi;
   int32_t rd_mode;
   int32_t scale_mode;
   float loss_scale;
+  int32_t ref_mode;
+  float alpha;
 } dppo_params;
 
 /*
@@ -130,7 +144,8 @@ dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V,
  *  logits        [T, ld] of dtype; dlogits (if non-NULL) [T, ld_dlogits] of the same
  *                dtype. dlogits may alias logits only exactly (same pointer and stride);
  *                any other overlap is DPPO_ERR_INVALID_ARG.
- *  token_ids     [T] int64.   logp_mu_old, logp_ref, advantages: [T] float32.
+ *  token_ids     [T] int64.   logp_mu_old, logp_ref, advantages: [T] float32; logp_ref
+ *                only with ref_mode GIVEN (NULL allowed otherwise).
  *  loss_mask     [T] uint8 or NULL (all 1). Rows with m_t = 0 are not read: lp 0, loss 0,
  *                flags 0, and a zero dlogits row.
  *  token_scale   [T] float32 or NULL (all 1).
@@ -182,6 +197,21 @@ dppo_status dppo_set_path_policy(int32_t policy);
  * next call on this host thread. NULL for an invalid dtype or V < 1 or ld < V. */
 const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t with_dlogits);
 
+/* Effective bounds on the total ratio r = pi_theta / mu_old that an interpolated
+ * reference induces (Prop. 1; App. A; Table 4): with the band [mask_lo, mask_hi] on r_d
+ * and the PPO interval [clip_lo, clip_hi] on r_s,
+ *   out[0], out[1]: the band as bounds on r;
+ *   out[2]:         the clip lower bound on r (applies to A < 0);
+ *   out[3]:         the clip upper bound on r (applies to A >= 0).
+ * ref_mode LOGLINEAR: r_d = r^(1-alpha), r_s = r^alpha.
+ * ref_mode LINEAR:    r_d = alpha + (1-alpha) r, r_s = r / (alpha + (1-alpha) r); a clip
+ *                     bound b with (1-alpha) b >= 1 is unreachable and reported as +inf.
+ * Pure host arithmetic in double. INVALID_ARG for ref_mode GIVEN or unknown, alpha outside
+ * (0, 1), bounds that are negative or out of order, or a NULL out.                      */
+dppo_status dppo_effective_thresholds(double mask_lo, double mask_hi, double clip_lo,
+                                      double clip_hi, double alpha, int32_t ref_mode,
+                                      double* out);
+
 /* Static description of a status code. */
 const char* dppo_strerror(dppo_status s);
 
@@ -189,7 +219,7 @@ const char* dppo_strerror(dppo_status s);
 const char* dppo_last_error(void);
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define DPPO_ABI_VERSION 1
+#define DPPO_ABI_VERSION 2
 int32_t dppo_abi_version(void);
 
 /*

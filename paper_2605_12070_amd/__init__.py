@@ -17,13 +17,13 @@ import torch
 
 from . import _lib
 from ._lib import (DppoError, FLAG_BAD_ID, FLAG_BAND, FLAG_PPO, FLAG_VALID,  # noqa: F401
-                   RD_MODES, SCALE_MODES, STAT_N_ACTIVE, STAT_N_BAD, STAT_N_BAND, STAT_N_PPO,
+                   RD_MODES, REF_MODES, SCALE_MODES, STAT_N_ACTIVE, STAT_N_BAD, STAT_N_BAND, STAT_N_PPO,
                    STAT_N_VALID)
 
 __all__ = [
     "logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "ewma_proxy_update", "LossResult",
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
-    "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name",
+    "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
 ]
 
 
@@ -86,17 +86,21 @@ class LossResult:
 def decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advantages,
                                loss_mask=None, token_scale=None, *, band=(0.5, 2.0),
                                clip_eps=(0.2, 0.2), rd_mode="mask_weight",
-                               scale_mode="token_mean", loss_scale=1.0, want_dlogits=True,
-                               dlogits=None, want_flags=True, out: LossResult | None = None
-                               ) -> LossResult:
+                               scale_mode="token_mean", loss_scale=1.0, ref_mode="given",
+                               alpha=0.5, want_dlogits=True, dlogits=None, want_flags=True,
+                               out: LossResult | None = None) -> LossResult:
     """Fused loss stage: log-prob, ratios, band and clip decisions, per-token loss, stats and
     dlogits = w (softmax - onehot). `dlogits` may be the logits tensor itself (in place) or
-    a preallocated tensor; `out` reuses all output buffers."""
+    a preallocated tensor; `out` reuses all output buffers. ref_mode "log_linear" or
+    "linear" interpolates the reference between mu_old (weight alpha) and the current
+    policy instead of reading logp_ref (which may then be None)."""
     ptr, T, V, ld = _matrix(logits, "logits")
     dev = logits.device
     ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
     mu = _vec(logp_mu_old, T, torch.float32, "logp_mu_old", dev)
-    ref = _vec(logp_ref, T, torch.float32, "logp_ref", dev)
+    if ref_mode not in REF_MODES:
+        raise ValueError(f"ref_mode in {list(REF_MODES)}")
+    ref = _vec(logp_ref, T, torch.float32, "logp_ref", dev, optional=ref_mode != "given")
     adv = _vec(advantages, T, torch.float32, "advantages", dev)
     msk = _vec(loss_mask, T, torch.uint8, "loss_mask", dev, optional=True)
     tsc = _vec(token_scale, T, torch.float32, "token_scale", dev, optional=True)
@@ -120,7 +124,8 @@ def decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advanta
         out.dlogits = None
         d_ptr, ldd = None, 0
     p = _lib.DppoParams(float(band[0]), float(band[1]), float(clip_eps[0]), float(clip_eps[1]),
-                        RD_MODES[rd_mode], SCALE_MODES[scale_mode], float(loss_scale))
+                        RD_MODES[rd_mode], SCALE_MODES[scale_mode], float(loss_scale),
+                        REF_MODES[ref_mode], float(alpha))
     st = _lib.lib().decoupled_ppo_loss_fwd_bwd(
         ptr, _dtype_code(logits), T, V, ld, ids, mu, ref, adv, msk, tsc, C.byref(p),
         out.logp.data_ptr(), out.loss_tok.data_ptr(), out.loss.data_ptr(),
@@ -151,6 +156,19 @@ def set_path_policy(policy: str):
     """'auto' (register-resident rows when they fit) or 'stream' (always two-pass)."""
     code = {"auto": 0, "stream": 1}[policy]
     _lib.check(_lib.lib().dppo_set_path_policy(code), "dppo_set_path_policy")
+
+
+def effective_thresholds(band, clip, alpha: float, kind: str):
+    """Bounds on the total ratio pi_theta / mu_old that an interpolated reference induces
+    (Prop. 1, App. A): returns ((band_lo, band_hi), (clip_lo, clip_hi)) on the total ratio
+    for the band `band` on r_d and the PPO interval `clip` = (1 - eps_lo, 1 + eps_hi) on r_s;
+    the clip lower bound applies to A < 0, the upper one to A >= 0."""
+    out = (C.c_double * 4)()
+    _lib.check(_lib.lib().dppo_effective_thresholds(float(band[0]), float(band[1]),
+                                                    float(clip[0]), float(clip[1]),
+                                                    float(alpha), REF_MODES[kind], out),
+               "dppo_effective_thresholds")
+    return (out[0], out[1]), (out[2], out[3])
 
 
 def row_kernel_name(dtype: torch.dtype, V: int, ld: int | None = None,

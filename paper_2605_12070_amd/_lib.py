@@ -15,10 +15,11 @@ DPPO_OK, DPPO_ERR_INVALID_ARG, DPPO_ERR_UNSUPPORTED, DPPO_ERR_HIP = 0, 1, 2, 3
 DPPO_F32, DPPO_BF16 = 0, 1
 RD_MODES = {"none": 0, "mask": 1, "weight": 2, "mask_weight": 3}
 SCALE_MODES = {"const": 0, "token_mean": 1}
+REF_MODES = {"given": 0, "log_linear": 1, "linear": 2}
 FLAG_VALID, FLAG_BAND, FLAG_PPO, FLAG_BAD_ID = 1, 2, 4, 8
 STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 # Every function the header declares, with its C signature.
 VP, I32, I64, F32, F64 = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double
@@ -28,7 +29,7 @@ class DppoParams(C.Structure):
     _fields_ = [("band_lo", C.c_float), ("band_hi", C.c_float),
                 ("clip_eps_lo", C.c_float), ("clip_eps_hi", C.c_float),
                 ("rd_mode", C.c_int32), ("scale_mode", C.c_int32),
-                ("loss_scale", C.c_float)]
+                ("loss_scale", C.c_float), ("ref_mode", C.c_int32), ("alpha", C.c_float)]
 
 
 SIGNATURES = {
@@ -43,6 +44,8 @@ SIGNATURES = {
     "dppo_timer_enable": (I32, [I32]),
     "dppo_timer_read": (I32, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "dppo_row_kernel_name": (C.c_char_p, [I32, I64, I64, I32]),
+    "dppo_effective_thresholds": (I32, [C.c_double, C.c_double, C.c_double, C.c_double,
+                                        C.c_double, I32, C.POINTER(C.c_double)]),
 }
 
 _lock = threading.Lock()

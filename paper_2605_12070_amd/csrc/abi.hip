@@ -206,6 +206,34 @@ const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t w
   return buf;
 }
 
+dppo_status dppo_effective_thresholds(double mask_lo, double mask_hi, double clip_lo,
+                                      double clip_hi, double alpha, int32_t ref_mode,
+                                      double* out) {
+  if (!out) return fail(DPPO_ERR_INVALID_ARG, "dppo_effective_thresholds: NULL out");
+  if (ref_mode != DPPO_REF_LOGLINEAR && ref_mode != DPPO_REF_LINEAR)
+    return fail(DPPO_ERR_INVALID_ARG, "ref_mode %d is not an interpolated reference", (int)ref_mode);
+  if (!(alpha > 0.0 && alpha < 1.0)) return fail(DPPO_ERR_INVALID_ARG, "alpha = %g not in (0, 1)", alpha);
+  if (!(mask_lo >= 0.0 && mask_lo <= mask_hi) || !(clip_lo >= 0.0 && clip_lo <= clip_hi))
+    return fail(DPPO_ERR_INVALID_ARG, "bounds must satisfy 0 <= lo <= hi");
+  if (ref_mode == DPPO_REF_LOGLINEAR) {
+    // r_d = r^(1 - alpha) and r_s = r^alpha are increasing in r: invert each bound.
+    out[0] = std::pow(mask_lo, 1.0 / (1.0 - alpha));
+    out[1] = std::pow(mask_hi, 1.0 / (1.0 - alpha));
+    out[2] = std::pow(clip_lo, 1.0 / alpha);
+    out[3] = std::pow(clip_hi, 1.0 / alpha);
+  } else {
+    // r_d = alpha + (1 - alpha) r is linear in r; r_s = r / (alpha + (1 - alpha) r) rises
+    // from 0 towards 1 / (1 - alpha), so r_s = b has the root alpha b / (1 - (1 - alpha) b)
+    // only below that limit; at or above it the bound is never reached.
+    out[0] = (mask_lo - alpha) / (1.0 - alpha);
+    out[1] = (mask_hi - alpha) / (1.0 - alpha);
+    const double lim = 1.0 / (1.0 - alpha);
+    out[2] = clip_lo < lim ? alpha * clip_lo / (1.0 - (1.0 - alpha) * clip_lo) : INFINITY;
+    out[3] = clip_hi < lim ? alpha * clip_hi / (1.0 - (1.0 - alpha) * clip_hi) : INFINITY;
+  }
+  return DPPO_OK;
+}
+
 dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                         const int64_t* token_ids, float* logp_out, float* lse_out, void* stream) {
   dppo_status s = check_matrix(logits, dtype, T, V, ld, "logits");
@@ -238,9 +266,16 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
   if (s != DPPO_OK) return s;
   if (!p) return fail(DPPO_ERR_INVALID_ARG, "params pointer is NULL");
   if (!loss_out || !stats_out) return fail(DPPO_ERR_INVALID_ARG, "loss_out and stats_out are required");
-  if (T > 0 && (!token_ids || !logp_mu_old || !logp_ref || !advantages || !logp_out || !loss_tok_out))
+  if (p->ref_mode < DPPO_REF_GIVEN || p->ref_mode > DPPO_REF_LINEAR)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown ref_mode %d", (int)p->ref_mode);
+  if (p->ref_mode != DPPO_REF_GIVEN && !(p->alpha > 0.0f && p->alpha < 1.0f))
+    return fail(DPPO_ERR_INVALID_ARG, "alpha = %g must lie in (0, 1) for an interpolated reference",
+                p->alpha);
+  if (T > 0 && (!token_ids || !logp_mu_old || !advantages || !logp_out || !loss_tok_out))
     return fail(DPPO_ERR_INVALID_ARG,
-                "token_ids, logp_mu_old, logp_ref, advantages, logp_out, loss_tok_out are required");
+                "token_ids, logp_mu_old, advantages, logp_out, loss_tok_out are required");
+  if (T > 0 && p->ref_mode == DPPO_REF_GIVEN && !logp_ref)
+    return fail(DPPO_ERR_INVALID_ARG, "logp_ref is required with ref_mode GIVEN");
   if (std::isnan(p->band_lo) || std::isnan(p->band_hi) || p->band_lo < 0.0f || p->band_lo > p->band_hi)
     return fail(DPPO_ERR_INVALID_ARG, "band [%g, %g] must satisfy 0 <= lo <= hi", p->band_lo, p->band_hi);
   if (!(p->clip_eps_lo >= 0.0f) || !(p->clip_eps_hi >= 0.0f) || !std::isfinite(p->clip_eps_lo) ||
@@ -274,7 +309,9 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
     a.ldd = ld_dlogits;
     a.ids = token_ids;
     a.lp_mu = logp_mu_old;
-    a.lp_ref = logp_ref;
+    a.lp_ref = p->ref_mode == DPPO_REF_GIVEN ? logp_ref : nullptr;
+    a.ref_mode = p->ref_mode;
+    a.alpha = p->alpha;
     a.adv = advantages;
     a.mask = loss_mask;
     a.tscale = token_scale;

@@ -37,6 +37,8 @@ struct RowArgs {
   float loss_scale;
   int32_t rd_mode;
   int32_t scale_mode;
+  int32_t ref_mode;     // dppo_ref_mode; lp_ref is NULL unless GIVEN
+  float alpha;          // behaviour-policy weight of an interpolated reference
 };
 
 typedef void (*RowKernel)(RowArgs);

@@ -39,7 +39,7 @@ __device__ __forceinline__ TokenIn token_inputs(const RowArgs& a, int64_t row) {
     t.ts = t.scale = 1.0f;
     return t;
   }
-  t.lp_ref = uload(a.lp_ref + row);
+  t.lp_ref = a.lp_ref ? uload(a.lp_ref + row) : 0.0f;
   t.lp_mu = uload(a.lp_mu + row);
   t.adv = uload(a.adv + row);
   t.ts = a.tscale ? uload(a.tscale + row) : 1.0f;
@@ -53,8 +53,17 @@ __device__ __forceinline__ TokenOut token_math(const RowArgs& a, const TokenIn& 
   const float lse = lse2 * kLn2;
   const float lp = zy - lse;
   o.lp = lp;
-  const float lp_ref = t.lp_ref;
   const float lp_mu = t.lp_mu;
+  float lp_ref = t.lp_ref;
+  if (a.ref_mode == DPPO_REF_LOGLINEAR) {
+    // App. A: log pi_ref = alpha log mu_old + (1 - alpha) log pi_theta
+    lp_ref = __builtin_fmaf(a.alpha, lp_mu, (1.0f - a.alpha) * lp);
+  } else if (a.ref_mode == DPPO_REF_LINEAR) {
+    // App. A: pi_ref = alpha mu_old + (1 - alpha) pi_theta, as a log-sum-exp of the two
+    // weighted terms around their larger log-prob
+    const float m = fmaxf(lp_mu, lp);
+    lp_ref = m + logf(a.alpha * expf(lp_mu - m) + (1.0f - a.alpha) * expf(lp - m));
+  }
   const float A = t.adv;
   const float ts = t.ts;
   const float scale = t.scale;

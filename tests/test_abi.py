@@ -64,10 +64,10 @@ def _params(**kw):
 
 
 def _loss(T=4, V=8, ld=8, dtype=1, p=None, dl=None, ldd=8, ids=FAKE, logits=FAKE, stats=FAKE,
-          loss=FAKE):
+          loss=FAKE, ref=FAKE):
     p = p or _params()
     L = _lib.lib()
-    return L.decoupled_ppo_loss_fwd_bwd(logits, dtype, T, V, ld, ids, FAKE, FAKE, FAKE, None,
+    return L.decoupled_ppo_loss_fwd_bwd(logits, dtype, T, V, ld, ids, FAKE, ref, FAKE, None,
                                         None, C.byref(p), FAKE, FAKE, loss, None, dl, ldd,
                                         stats, None)
 
@@ -89,6 +89,11 @@ def _loss(T=4, V=8, ld=8, dtype=1, p=None, dl=None, ldd=8, ids=FAKE, logits=FAKE
     (dict(p=_params(loss_scale=float("nan"))), "loss_scale"),
     (dict(p=_params(rd_mode=9)), "rd_mode"),
     (dict(p=_params(scale_mode=5)), "scale_mode"),
+    (dict(p=_params(ref_mode=3, alpha=0.5)), "ref_mode"),
+    (dict(p=_params(ref_mode=1, alpha=0.0)), "alpha"),
+    (dict(p=_params(ref_mode=2, alpha=1.0)), "alpha"),
+    (dict(p=_params(ref_mode=1, alpha=float("nan"))), "alpha"),
+    (dict(ref=None), "logp_ref is required"),
     (dict(dl=FAKE + 2 * 8, ldd=8), "overlaps"),        # dlogits overlaps logits, not equal
     (dict(dl=FAKE, ldd=16, ld=8), "overlaps"),          # same base, different stride
     (dict(dl=FAKE + 64, ldd=4), "stride"),
@@ -199,3 +204,68 @@ def test_row_kernel_name_follows_the_selection_rule():
     assert L.dppo_row_kernel_name(7, 100, 100, 1) is None
     assert L.dppo_row_kernel_name(1, 0, 0, 1) is None
     assert L.dppo_row_kernel_name(1, 100, 99, 1) is None
+
+
+# ---------------------------------------------------------------------- effective thresholds
+GOLDEN4 = os.path.join(ROOT, "tests", "golden", "table4_effective_thresholds.csv")
+
+
+def _table4():
+    import csv
+    with open(GOLDEN4) as f:
+        return list(csv.DictReader(l for l in f if not l.startswith("#")))
+
+
+@pytest.mark.parametrize("row", _table4(), ids=lambda r: f"{r['mask_lo']}-{r['clip_hi']}-n{r['n']}-{r['kind']}")
+def test_effective_thresholds_match_table4(row):
+    """The library's host helper reproduces every printed entry of Table 4 (App. A)."""
+    from paper_2605_12070_amd import effective_thresholds
+    alpha = 1.0 / (int(row["n"]) + 1)
+    m, c = effective_thresholds((float(row["mask_lo"]), float(row["mask_hi"])),
+                                (float(row["clip_lo"]), float(row["clip_hi"])), alpha, row["kind"])
+    want = [float(row[k]) for k in ("eff_mask_lo", "eff_mask_hi", "eff_clip_lo", "eff_clip_hi")]
+    for g, w in zip([*m, *c], want):
+        assert abs(g - w) <= 0.5e-4 + 1e-12, (g, w)
+
+
+@pytest.mark.parametrize("kind", ["log_linear", "linear"])
+def test_effective_thresholds_match_the_oracle(kind):
+    import numpy as np
+    import oracle
+    from paper_2605_12070_amd import effective_thresholds
+    rng = np.random.default_rng(3)
+    for _ in range(200):
+        alpha = rng.uniform(0.05, 0.95)
+        m_lo, m_hi = np.sort(rng.uniform(0.3, 2.0, size=2))
+        c_lo, c_hi = rng.uniform(0.5, 1.0), rng.uniform(1.0, 1.0 / (1.0 - alpha) - 1e-3)
+        got = effective_thresholds((m_lo, m_hi), (c_lo, c_hi), alpha, kind)
+        ref = oracle.effective_thresholds(m_lo, m_hi, c_lo, c_hi, alpha, kind)
+        np.testing.assert_allclose(np.array(got).ravel(), np.array(ref).ravel(), rtol=1e-12)
+
+
+def test_linear_clip_bound_beyond_reach_is_infinite():
+    """With pi_ref = alpha mu + (1 - alpha) pi_theta, r_s = r / (alpha + (1 - alpha) r) never
+    exceeds 1 / (1 - alpha): a clip bound at or above that never binds."""
+    import numpy as np
+    from paper_2605_12070_amd import effective_thresholds
+    alpha = 0.25
+    (_, _), (lo, hi) = effective_thresholds((0.5, 2.0), (0.9, 1.0 / (1 - alpha)), alpha, "linear")
+    assert hi == float("inf") and np.isfinite(lo)
+    r = np.logspace(-6, 6, 1001)
+    assert np.all(r / (alpha + (1 - alpha) * r) <= 1.0 / (1 - alpha))
+
+
+@pytest.mark.parametrize("args,frag", [
+    ((0.9, 1.1, 0.8, 1.2, 0.5, 0), "not an interpolated"),
+    ((0.9, 1.1, 0.8, 1.2, 0.5, 7), "not an interpolated"),
+    ((0.9, 1.1, 0.8, 1.2, 0.0, 1), "alpha"),
+    ((0.9, 1.1, 0.8, 1.2, 1.0, 2), "alpha"),
+    ((1.2, 1.1, 0.8, 1.2, 0.5, 1), "bounds"),
+    ((0.9, 1.1, -0.1, 1.2, 0.5, 2), "bounds"),
+])
+def test_effective_thresholds_reject_bad_arguments(args, frag):
+    out = (C.c_double * 4)()
+    assert _lib.lib().dppo_effective_thresholds(*args, out) == _lib.DPPO_ERR_INVALID_ARG
+    assert frag in _lib.lib().dppo_last_error().decode()
+    assert _lib.lib().dppo_effective_thresholds(0.9, 1.1, 0.8, 1.2, 0.5, 1, None) == \
+        _lib.DPPO_ERR_INVALID_ARG

@@ -307,3 +307,41 @@ def test_forward_only_and_autograd_wrapper():
     (2.0 * loss).backward()
     torch.cuda.synchronize()
     assert torch.allclose(z.grad, 2.0 * both.dlogits, rtol=0, atol=0)
+
+
+@pytest.mark.parametrize("kind", ["log_linear", "linear"])
+@pytest.mark.parametrize("wl_name,T,n_gap,band,eps", [
+    ("tiny", None, 1, (0.5, 2.0), (0.2, 0.2)),
+    ("large_vocab", 64, 1, (0.99, 1.01), (0.003, 0.004)),      # Table 4, first block
+    ("large_vocab", 64, 3, (1 / 1.003, 1.003), (0.006, 0.006)),
+])
+def test_interpolated_reference(kind, wl_name, T, n_gap, band, eps):
+    """ref_mode log_linear / linear (App. A): the kernel builds pi_ref from mu_old and its own
+    log-prob; the oracle takes the same proxy of its own float64 log-prob. Then Prop. 1 through
+    the kernel: its kept tokens are those whose total ratio lies inside the effective bounds
+    that the library's threshold helper reports."""
+    alpha = 1.0 / (n_gap + 1)
+    _say("interpolated ref", kind, wl_name, T, alpha, band, eps)
+    wl = W.make_workload(wl_name, device=DEV, T=T, seq_len=8 if T else None)
+    anchor = oracle_anchor(wl.logits, wl.ids)                 # oracle lp, float64
+    _, lp_mu = W.reference_logprobs(anchor.to(DEV), wl)
+    res = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, None, wl.adv, wl.mask,
+                                       band=band, clip_eps=eps, ref_mode=kind, alpha=alpha)
+    torch.cuda.synchronize()
+    proxy = (oracle.log_linear_proxy_logprob if kind == "log_linear"
+             else oracle.linear_proxy_logprob)(lp_mu.cpu().double().numpy(), anchor.numpy(), alpha)
+    params = oracle_params(band, eps, "mask_weight", "token_mean", 1.0)
+    ref = run_oracle(wl.logits, wl.ids, lp_mu, torch.from_numpy(proxy), wl.adv, wl.mask, None,
+                     params)
+    n_ties = compare_loss(res, ref, params, wl.logits.dtype)
+    # Prop. 1: band and PPO decisions on the decoupled ratios = bounds on the total ratio
+    m, c = P.effective_thresholds(band, (1 - eps[0], 1 + eps[1]), alpha, kind)
+    r = np.exp(anchor.numpy() - lp_mu.cpu().double().numpy())
+    adv = wl.adv.cpu().numpy()
+    keep_eff = (r >= m[0]) & (r <= m[1]) & np.where(adv >= 0, r <= c[1], r >= c[0])
+    fl = res.flags.cpu().numpy()
+    keep = ((fl & P.FLAG_BAND) != 0) & ((fl & P.FLAG_PPO) != 0)
+    bounds = np.log(np.array([b for b in (*m, *c) if np.isfinite(b) and b > 0]))
+    edge = np.min(np.abs(np.log(r)[:, None] - bounds[None]), axis=1) < 1e-4
+    assert np.array_equal(keep[~edge], keep_eff[~edge])
+    _say("interpolated ref ok", kind, wl_name, "ties", n_ties, "kept", int(keep.sum()), "of", len(keep))
