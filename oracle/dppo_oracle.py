@@ -434,3 +434,31 @@ def effective_thresholds(mask_lo, mask_hi, clip_lo, clip_hi, alpha, kind):
     else:
         raise ValueError(f"unknown interpolation kind {kind!r}")
     return m, c
+
+
+# ---------------------------------------------------------------------------------------
+# Loss stage with the LM head folded in
+# ---------------------------------------------------------------------------------------
+def lm_head_loss(hidden, weight, ids, lp_mu, lp_ref, adv, mask=None, token_scale=None,
+                 params: Params = Params(), want_grads: bool = True):
+    """The loss stage on logits z = hidden @ weight^T, with gradients for both factors.
+
+    hidden [T, d] and weight [V, d] are float arrays (decode bfloat16 with
+    bf16_bits_to_f64); weight is the LM head in the [out, in] layout, so row v of weight
+    produces logit v. The logits are formed with one float64 matrix product, the loss stage
+    is decoupled_ppo_loss on them, and the chain rule through z = hidden weight^T gives
+        d L / d hidden = dlogits @ weight,     d L / d weight = dlogits^T @ hidden.
+    Returns decoupled_ppo_loss's dict plus "dhidden" [T, d] and "dweight" [V, d] when
+    want_grads. lp_ref may be an interpolated proxy computed by the caller (App. A).
+    """
+    h = as_f64(hidden)
+    wt = as_f64(weight)
+    z = h @ wt.T
+    out = decoupled_ppo_loss(z, ids, lp_mu, lp_ref, adv, mask, token_scale, params,
+                             want_dlogits=want_grads)
+    out["logits"] = z
+    if want_grads:
+        g = out["dlogits"]
+        out["dhidden"] = g @ wt
+        out["dweight"] = g.T @ h
+    return out
