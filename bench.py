@@ -39,7 +39,7 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-KERNEL_SOURCES = ("dppo_device.h", "loss_stage.h", "loss_stage.hip")
+KERNEL_SOURCES = ("dppo_device.h", "loss_stage.h", "token_math.h", "loss_stage.hip")
 
 
 def kernel_source_hash() -> str:
@@ -145,6 +145,52 @@ def ewma_bandwidth(dev, n, reps=20):
             "n": n, "dtype": "f32", "alg_bytes_per_launch": 12 * n, "kernel_ms": round(ms, 4)}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, AMD specification
+
+
+def lm_head_measure(dev, reps=5):
+    """Fused LM-head loss stage (hidden [8192, 4096] x weight [151936, 4096]^T, bf16, logits
+    never materialised) with both gradients: per-call time and the matrix-core rate of the
+    library's own tile kernels (forward and backward launches, 2 T d V flops each)."""
+    wl = W.make_lm_head_workload(dev)
+    T, V, d = wl.T, wl.V, wl.hidden.shape[1]
+    anchor = torch.empty(T, dtype=torch.float64, device=dev)
+    for a in range(0, T, 512):           # input synthesis only (reference log-probs)
+        z = wl.hidden[a:a + 512].float() @ wl.weight.float().T
+        anchor[a:a + 512] = (z.gather(1, wl.ids[a:a + 512, None])[:, 0]
+                             - torch.logsumexp(z, dim=1)).double()
+        del z
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    out = None
+    for _ in range(2):
+        out = P.fused_lm_head_loss_fwd_bwd(wl.hidden, wl.weight, wl.ids, lp_mu, lp_ref, wl.adv,
+                                           wl.mask, out=out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with P.KernelTimer() as kt:
+        e0.record(stream)
+        for _ in range(reps):
+            out = P.fused_lm_head_loss_fwd_bwd(wl.hidden, wl.weight, wl.ids, lp_mu, lp_ref,
+                                               wl.adv, wl.mask, out=out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        k_ms, k_n = kt.read()
+    call_ms = e0.elapsed_time(e1) / reps
+    tile_ms = k_ms / max(1, k_n)
+    tile_flops = 2.0 * T * d * V
+    achieved = tile_flops / (tile_ms * 1e-3) / 1e12
+    total_flops = 8.0 * T * d * V
+    del out, wl
+    return {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "kernel": "dppo::lmh_fwd_tiles / dppo::lmh_bwd_tiles", "kernel_ms": round(tile_ms, 3),
+            "alg_flops_per_launch": tile_flops,
+            "workload": f"lm_head T={T} d={d} V={V} bf16, both gradients",
+            "call_ms": round(call_ms, 3), "tokens_per_s": round(T / (call_ms * 1e-3), 1),
+            "call_tflops": round(total_flops / (call_ms * 1e-3) / 1e12, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -156,6 +202,8 @@ def main():
     ap.add_argument("--no-copy", action="store_true")
     ap.add_argument("--ewma-elems", type=int, default=1 << 30,
                     help="size of the parameter-sized EWMA measurement (0 to skip)")
+    ap.add_argument("--no-lm-head", action="store_true",
+                    help="skip the fused LM-head measurement")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -246,6 +294,9 @@ def main():
     }
     if args.ewma_elems > 0:
         result["ewma_roofline"] = ewma_bandwidth(dev, args.ewma_elems)
+    if not args.no_lm_head:
+        log("fused LM head")
+        result["lm_head_roofline"] = lm_head_measure(dev)
     if not args.no_copy:
         result["context"] = {"d2d_copy_GBps": round(copy_bandwidth(dev), 1)}
     if not args.no_cpu_baseline:

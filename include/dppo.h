@@ -167,6 +167,44 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
     uint8_t* flags_out, void* dlogits, int64_t ld_dlogits, int32_t* stats_out, void* stream);
 
 /*
+ * fused_lm_head_loss_fwd_bwd -- decoupled_ppo_loss_fwd_bwd on logits z = hidden weight^T
+ * that are never written to memory, with the gradients of L for both factors:
+ *     d L / d hidden = G weight,   d L / d weight = G^T hidden,
+ *     G[t, v] = w_t (softmax(z_t)[v] - 1{v = y_t})   (the dlogits of the row entry point).
+ * The logits exist only as 128 x 128 tiles in registers and LDS, formed with bf16 matrix-core
+ * products and fp32 accumulation; the forward pass reduces each tile to a per-token partial
+ * log-sum-exp, the backward pass recomputes the tiles and writes G in bf16 one vocabulary
+ * chunk at a time into the workspace, and the two gradient products (plain GEMMs, fp32
+ * results) run in rocBLAS. lp, loss, flags, stats and the parameters are as in
+ * decoupled_ppo_loss_fwd_bwd (ref_mode included).
+ *
+ *  hidden       [T, d] bf16, row-major, 16-byte aligned.
+ *  weight       [V, d] bf16, row-major (an LM head in the [out, in] layout), 16-byte aligned.
+ *  dtype        DPPO_BF16 (DPPO_F32 is DPPO_ERR_UNSUPPORTED).
+ *  d            multiple of 8, at most 2^20; V < 2^23; T < 2^31.
+ *  dhidden      [T, d] float32 or NULL (not computed); overwritten.
+ *  dweight      [V, d] float32 or NULL (not computed); overwritten.
+ *  vocab_chunk  vocabulary rows per backward chunk (rounded up to 128); <= 0 means all of V.
+ *  workspace    device buffer of at least fused_lm_head_workspace_bytes(T, d, V, vocab_chunk)
+ *               bytes, 256-byte aligned, owned by the caller; its contents are scratch.
+ * Masked rows and bad ids behave as in the row entry point (their G rows are zero). The
+ * computation of rows with loss mask 0 is not skipped. rocBLAS is initialised on the first
+ * call on a device (one handle per device, kept for the process).
+ */
+dppo_status fused_lm_head_loss_fwd_bwd(
+    const void* hidden, const void* weight, int32_t dtype, int64_t T, int64_t d, int64_t V,
+    const int64_t* token_ids, const float* logp_mu_old, const float* logp_ref,
+    const float* advantages, const uint8_t* loss_mask, const float* token_scale,
+    const dppo_params* p, float* logp_out, float* loss_tok_out, float* loss_out,
+    uint8_t* flags_out, int32_t* stats_out, float* dhidden, float* dweight,
+    int64_t vocab_chunk, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Workspace bytes fused_lm_head_loss_fwd_bwd needs for these sizes (-1 if they are out of
+ * range): per-token partial sums of every 128-entry vocabulary tile (8 B per token and
+ * tile), four per-token vectors and one bf16 [T, vocab_chunk] gradient chunk. */
+int64_t fused_lm_head_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t vocab_chunk);
+
+/*
  * ewma_proxy_update -- one step of the PPO-EWMA reference (Sec. 5.2, Eq. 5; App. B) on a
  * flat buffer of n elements (proxy parameters, or per-token log-probs).
  *  normalized = 1: w_t = 1 + beta * w_{t-1};

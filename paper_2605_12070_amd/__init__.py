@@ -24,6 +24,7 @@ __all__ = [
     "logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "ewma_proxy_update", "LossResult",
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
     "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
+    "fused_lm_head_loss_fwd_bwd", "LmHeadResult", "lm_head_workspace_bytes",
 ]
 
 
@@ -132,6 +133,77 @@ def decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advanta
         out.flags.data_ptr() if out.flags is not None else None, d_ptr, ldd,
         out.stats.data_ptr(), _stream(dev))
     _lib.check(st, "decoupled_ppo_loss_fwd_bwd")
+    return out
+
+
+@dataclass
+class LmHeadResult:
+    loss: torch.Tensor          # [1] fp32
+    logp: torch.Tensor          # [T] fp32
+    loss_tok: torch.Tensor      # [T] fp32
+    flags: torch.Tensor | None  # [T] uint8
+    stats: torch.Tensor         # [5] int32
+    dhidden: torch.Tensor | None  # [T, d] fp32
+    dweight: torch.Tensor | None  # [V, d] fp32
+    workspace: torch.Tensor     # scratch, reusable by the next call (out=)
+
+
+def lm_head_workspace_bytes(T: int, d: int, V: int, vocab_chunk: int = 0) -> int:
+    n = _lib.lib().fused_lm_head_workspace_bytes(T, d, V, vocab_chunk)
+    if n < 0:
+        raise ValueError(f"sizes out of range: T={T}, d={d}, V={V}")
+    return n
+
+
+def fused_lm_head_loss_fwd_bwd(hidden, weight, token_ids, logp_mu_old, logp_ref, advantages,
+                               loss_mask=None, token_scale=None, *, band=(0.5, 2.0),
+                               clip_eps=(0.2, 0.2), rd_mode="mask_weight",
+                               scale_mode="token_mean", loss_scale=1.0, ref_mode="given",
+                               alpha=0.5, want_grads=True, vocab_chunk=0, want_flags=True,
+                               out: LmHeadResult | None = None) -> LmHeadResult:
+    """The loss stage on logits hidden @ weight.T (never materialised), with d L / d hidden
+    and d L / d weight. hidden [T, d] and weight [V, d] are contiguous bf16 GPU tensors."""
+    for t, name in ((hidden, "hidden"), (weight, "weight")):
+        if t.dtype != torch.bfloat16 or t.dim() != 2 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"{name} must be a contiguous 2-D bf16 GPU tensor")
+    T, d = hidden.shape
+    V = weight.shape[0]
+    if weight.shape[1] != d:
+        raise ValueError("hidden and weight disagree on d")
+    dev = hidden.device
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    mu = _vec(logp_mu_old, T, torch.float32, "logp_mu_old", dev)
+    if ref_mode not in REF_MODES:
+        raise ValueError(f"ref_mode in {list(REF_MODES)}")
+    ref = _vec(logp_ref, T, torch.float32, "logp_ref", dev, optional=ref_mode != "given")
+    adv = _vec(advantages, T, torch.float32, "advantages", dev)
+    msk = _vec(loss_mask, T, torch.uint8, "loss_mask", dev, optional=True)
+    tsc = _vec(token_scale, T, torch.float32, "token_scale", dev, optional=True)
+    if rd_mode not in RD_MODES or scale_mode not in SCALE_MODES:
+        raise ValueError(f"rd_mode in {list(RD_MODES)}, scale_mode in {list(SCALE_MODES)}")
+    nws = lm_head_workspace_bytes(T, d, V, vocab_chunk)
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=dev)
+        out = LmHeadResult(
+            loss=torch.empty(1, **f32), logp=torch.empty(T, **f32), loss_tok=torch.empty(T, **f32),
+            flags=torch.empty(T, dtype=torch.uint8, device=dev) if want_flags else None,
+            stats=torch.empty(_lib.N_STATS, dtype=torch.int32, device=dev),
+            dhidden=torch.empty(T, d, **f32) if want_grads else None,
+            dweight=torch.empty(V, d, **f32) if want_grads else None,
+            workspace=torch.empty(max(nws, 1), dtype=torch.uint8, device=dev))
+    if out.workspace.numel() < nws:
+        out.workspace = torch.empty(nws, dtype=torch.uint8, device=dev)
+    p = _lib.DppoParams(float(band[0]), float(band[1]), float(clip_eps[0]), float(clip_eps[1]),
+                        RD_MODES[rd_mode], SCALE_MODES[scale_mode], float(loss_scale),
+                        REF_MODES[ref_mode], float(alpha))
+    st = _lib.lib().fused_lm_head_loss_fwd_bwd(
+        hidden.data_ptr(), weight.data_ptr(), _lib.DTYPE_BF16, T, d, V, ids, mu, ref, adv, msk,
+        tsc, C.byref(p), out.logp.data_ptr(), out.loss_tok.data_ptr(), out.loss.data_ptr(),
+        out.flags.data_ptr() if out.flags is not None else None, out.stats.data_ptr(),
+        out.dhidden.data_ptr() if out.dhidden is not None else None,
+        out.dweight.data_ptr() if out.dweight is not None else None,
+        int(vocab_chunk), out.workspace.data_ptr(), out.workspace.numel(), _stream(dev))
+    _lib.check(st, "fused_lm_head_loss_fwd_bwd")
     return out
 
 

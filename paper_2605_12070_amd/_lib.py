@@ -19,6 +19,7 @@ REF_MODES = {"given": 0, "log_linear": 1, "linear": 2}
 FLAG_VALID, FLAG_BAND, FLAG_PPO, FLAG_BAD_ID = 1, 2, 4, 8
 STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
+DTYPE_F32, DTYPE_BF16 = 0, 1
 ABI_VERSION = 2
 
 # Every function the header declares, with its C signature.
@@ -44,6 +45,10 @@ SIGNATURES = {
     "dppo_timer_enable": (I32, [I32]),
     "dppo_timer_read": (I32, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     "dppo_row_kernel_name": (C.c_char_p, [I32, I64, I64, I32]),
+    "fused_lm_head_loss_fwd_bwd": (I32, [VP, VP, I32, I64, I64, I64, VP, VP, VP, VP, VP, VP,
+                                         C.POINTER(DppoParams), VP, VP, VP, VP, VP, VP, VP,
+                                         I64, VP, I64, VP]),
+    "fused_lm_head_workspace_bytes": (I64, [I64, I64, I64, I64]),
     "dppo_effective_thresholds": (I32, [C.c_double, C.c_double, C.c_double, C.c_double,
                                         C.c_double, I32, C.POINTER(C.c_double)]),
 }

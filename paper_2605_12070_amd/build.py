@@ -21,7 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdppo.so")
-SOURCES = ["loss_stage.hip", "ewma.hip", "abi.hip"]
+SOURCES = ["loss_stage.hip", "lm_head.hip", "ewma.hip", "abi.hip"]
 ARCH = "gfx950"
 
 FLAGS = [
@@ -29,6 +29,11 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
+
+
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+# rocBLAS runs the two plain gradient GEMMs of the fused LM head
+LINK = [f"-L{ROCM}/lib", "-lrocblas", f"-Wl,-rpath,{ROCM}/lib"]
 
 
 def hipcc() -> str:
@@ -62,7 +67,7 @@ def build(verbose: bool = False) -> str:
                 print(" ".join(cmd), flush=True)
             fut.result()
     tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp, *LINK])
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}", flush=True)

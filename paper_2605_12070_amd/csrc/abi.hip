@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -11,7 +12,10 @@
 
 #include "dppo.h"
 #include "ewma.h"
+#include "lm_head.h"
 #include "loss_stage.h"
+
+#include <rocblas/rocblas.h>
 
 namespace {
 
@@ -131,6 +135,80 @@ dppo_status check_matrix(const void* p, int32_t dtype, int64_t T, int64_t V, int
   if (V < 1 || V > 0x7FFFFFFF) return fail(DPPO_ERR_INVALID_ARG, "V = %lld out of [1, 2^31)", (long long)V);
   if (ld < V) return fail(DPPO_ERR_INVALID_ARG, "%s stride %lld < V = %lld", name, (long long)ld, (long long)V);
   if (T > 0 && p == nullptr) return fail(DPPO_ERR_INVALID_ARG, "%s is NULL", name);
+  return DPPO_OK;
+}
+
+// One rocBLAS handle per device, created on first use and kept for the process.
+rocblas_status blas_handle(rocblas_handle* out) {
+  static std::mutex mu;
+  static std::vector<std::pair<int, rocblas_handle>> handles;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return rocblas_status_internal_error;
+  std::lock_guard<std::mutex> lk(mu);
+  for (auto& h : handles)
+    if (h.first == dev) {
+      *out = h.second;
+      return rocblas_status_success;
+    }
+  rocblas_handle h = nullptr;
+  const rocblas_status st = rocblas_create_handle(&h);
+  if (st != rocblas_status_success) return st;
+  handles.push_back({dev, h});
+  *out = h;
+  return rocblas_status_success;
+}
+
+struct LmhLayout {
+  int64_t part, zy, w, lse2, ev, g, total;  // byte offsets into the workspace, and its size
+  int64_t chunk, ldg;                        // vocabulary rows per backward chunk, g's stride
+};
+
+int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+LmhLayout lmh_layout(int64_t T, int64_t V, int64_t vocab_chunk) {
+  LmhLayout L;
+  const int64_t ntiles = (V + dppo::LMH_BN - 1) / dppo::LMH_BN;
+  int64_t chunk = vocab_chunk <= 0 ? V : vocab_chunk;
+  chunk = ((chunk + dppo::LMH_BN - 1) / dppo::LMH_BN) * dppo::LMH_BN;
+  if (chunk > ntiles * dppo::LMH_BN) chunk = ntiles * dppo::LMH_BN;
+  L.chunk = chunk;
+  L.ldg = chunk;
+  int64_t o = 0;
+  L.part = o; o = align256(o + ntiles * T * 2 * 4);
+  L.zy = o;   o = align256(o + T * 4);
+  L.w = o;    o = align256(o + T * 4);
+  L.lse2 = o; o = align256(o + T * 4);
+  L.ev = o;   o = align256(o + T);
+  L.g = o;    o = align256(o + T * chunk * 2);
+  L.total = o;
+  return L;
+}
+
+// Parameters and per-token pointers shared by the loss entry points.
+dppo_status check_token_args(const dppo_params* p, int64_t T, const int64_t* token_ids,
+                             const float* logp_mu_old, const float* logp_ref,
+                             const float* advantages, const float* logp_out,
+                             const float* loss_tok_out) {
+  if (p->ref_mode < DPPO_REF_GIVEN || p->ref_mode > DPPO_REF_LINEAR)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown ref_mode %d", (int)p->ref_mode);
+  if (p->ref_mode != DPPO_REF_GIVEN && !(p->alpha > 0.0f && p->alpha < 1.0f))
+    return fail(DPPO_ERR_INVALID_ARG, "alpha = %g must lie in (0, 1) for an interpolated reference",
+                p->alpha);
+  if (T > 0 && (!token_ids || !logp_mu_old || !advantages || !logp_out || !loss_tok_out))
+    return fail(DPPO_ERR_INVALID_ARG,
+                "token_ids, logp_mu_old, advantages, logp_out, loss_tok_out are required");
+  if (T > 0 && p->ref_mode == DPPO_REF_GIVEN && !logp_ref)
+    return fail(DPPO_ERR_INVALID_ARG, "logp_ref is required with ref_mode GIVEN");
+  if (std::isnan(p->band_lo) || std::isnan(p->band_hi) || p->band_lo < 0.0f || p->band_lo > p->band_hi)
+    return fail(DPPO_ERR_INVALID_ARG, "band [%g, %g] must satisfy 0 <= lo <= hi", p->band_lo, p->band_hi);
+  if (!(p->clip_eps_lo >= 0.0f) || !(p->clip_eps_hi >= 0.0f) || !std::isfinite(p->clip_eps_lo) ||
+      !std::isfinite(p->clip_eps_hi))
+    return fail(DPPO_ERR_INVALID_ARG, "clip eps (%g, %g) must be finite and >= 0", p->clip_eps_lo, p->clip_eps_hi);
+  if (!std::isfinite(p->loss_scale)) return fail(DPPO_ERR_INVALID_ARG, "loss_scale must be finite");
+  if (p->rd_mode < DPPO_RD_NONE || p->rd_mode > DPPO_RD_MASK_WEIGHT)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown rd_mode %d", (int)p->rd_mode);
+  if (p->scale_mode != DPPO_SCALE_CONST && p->scale_mode != DPPO_SCALE_TOKEN_MEAN)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown scale_mode %d", (int)p->scale_mode);
   return DPPO_OK;
 }
 
@@ -266,26 +344,8 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
   if (s != DPPO_OK) return s;
   if (!p) return fail(DPPO_ERR_INVALID_ARG, "params pointer is NULL");
   if (!loss_out || !stats_out) return fail(DPPO_ERR_INVALID_ARG, "loss_out and stats_out are required");
-  if (p->ref_mode < DPPO_REF_GIVEN || p->ref_mode > DPPO_REF_LINEAR)
-    return fail(DPPO_ERR_INVALID_ARG, "unknown ref_mode %d", (int)p->ref_mode);
-  if (p->ref_mode != DPPO_REF_GIVEN && !(p->alpha > 0.0f && p->alpha < 1.0f))
-    return fail(DPPO_ERR_INVALID_ARG, "alpha = %g must lie in (0, 1) for an interpolated reference",
-                p->alpha);
-  if (T > 0 && (!token_ids || !logp_mu_old || !advantages || !logp_out || !loss_tok_out))
-    return fail(DPPO_ERR_INVALID_ARG,
-                "token_ids, logp_mu_old, advantages, logp_out, loss_tok_out are required");
-  if (T > 0 && p->ref_mode == DPPO_REF_GIVEN && !logp_ref)
-    return fail(DPPO_ERR_INVALID_ARG, "logp_ref is required with ref_mode GIVEN");
-  if (std::isnan(p->band_lo) || std::isnan(p->band_hi) || p->band_lo < 0.0f || p->band_lo > p->band_hi)
-    return fail(DPPO_ERR_INVALID_ARG, "band [%g, %g] must satisfy 0 <= lo <= hi", p->band_lo, p->band_hi);
-  if (!(p->clip_eps_lo >= 0.0f) || !(p->clip_eps_hi >= 0.0f) || !std::isfinite(p->clip_eps_lo) ||
-      !std::isfinite(p->clip_eps_hi))
-    return fail(DPPO_ERR_INVALID_ARG, "clip eps (%g, %g) must be finite and >= 0", p->clip_eps_lo, p->clip_eps_hi);
-  if (!std::isfinite(p->loss_scale)) return fail(DPPO_ERR_INVALID_ARG, "loss_scale must be finite");
-  if (p->rd_mode < DPPO_RD_NONE || p->rd_mode > DPPO_RD_MASK_WEIGHT)
-    return fail(DPPO_ERR_INVALID_ARG, "unknown rd_mode %d", (int)p->rd_mode);
-  if (p->scale_mode != DPPO_SCALE_CONST && p->scale_mode != DPPO_SCALE_TOKEN_MEAN)
-    return fail(DPPO_ERR_INVALID_ARG, "unknown scale_mode %d", (int)p->scale_mode);
+  s = check_token_args(p, T, token_ids, logp_mu_old, logp_ref, advantages, logp_out, loss_tok_out);
+  if (s != DPPO_OK) return s;
   const int es = esize_of(dtype);
   if (dlogits && T > 0) {
     if (ld_dlogits < V)
@@ -331,6 +391,146 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
     a.scale_mode = p->scale_mode;
     s = launch_rows(L, a, T, st);
     if (s != DPPO_OK) return s;
+  }
+  dppo::launch_loss_sum(loss_tok_out, loss_mask, token_scale, stats_out, T, p->loss_scale,
+                        p->scale_mode, loss_out, st);
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "loss_sum launch");
+  return DPPO_OK;
+}
+
+int64_t fused_lm_head_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t vocab_chunk) {
+  if (T < 0 || d < 8 || V < 1 || T >= ((int64_t)1 << 31) || V >= ((int64_t)1 << 31)) return -1;
+  return lmh_layout(T, V, vocab_chunk).total;
+}
+
+dppo_status fused_lm_head_loss_fwd_bwd(
+    const void* hidden, const void* weight, int32_t dtype, int64_t T, int64_t d, int64_t V,
+    const int64_t* token_ids, const float* logp_mu_old, const float* logp_ref,
+    const float* advantages, const uint8_t* loss_mask, const float* token_scale,
+    const dppo_params* p, float* logp_out, float* loss_tok_out, float* loss_out,
+    uint8_t* flags_out, int32_t* stats_out, float* dhidden, float* dweight,
+    int64_t vocab_chunk, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (dtype != DPPO_BF16 && dtype != DPPO_F32)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (dtype != DPPO_BF16)
+    return fail(DPPO_ERR_UNSUPPORTED, "the fused LM head takes bf16 hidden states and weights");
+  if (T < 0 || T >= ((int64_t)1 << 31)) return fail(DPPO_ERR_INVALID_ARG, "T = %lld out of range", (long long)T);
+  if (V < 1 || V >= ((int64_t)1 << 23)) return fail(DPPO_ERR_INVALID_ARG, "V = %lld out of range", (long long)V);
+  if (d < 8 || d % 8 != 0 || d > (1 << 20))
+    return fail(DPPO_ERR_INVALID_ARG, "d = %lld must be a multiple of 8 in [8, 2^20]", (long long)d);
+  if (!p) return fail(DPPO_ERR_INVALID_ARG, "params pointer is NULL");
+  if (!loss_out || !stats_out) return fail(DPPO_ERR_INVALID_ARG, "loss_out and stats_out are required");
+  if (!weight || !aligned16(weight) || (T > 0 && (!hidden || !aligned16(hidden))))
+    return fail(DPPO_ERR_INVALID_ARG, "hidden and weight must be non-NULL and 16-byte aligned");
+  dppo_status s = check_token_args(p, T, token_ids, logp_mu_old, logp_ref, advantages, logp_out,
+                                   loss_tok_out);
+  if (s != DPPO_OK) return s;
+  const LmhLayout L = lmh_layout(T, V, vocab_chunk);
+  if (T > 0 && (!workspace || workspace_bytes < L.total))
+    return fail(DPPO_ERR_INVALID_ARG, "workspace of %lld bytes needed, %lld given", (long long)L.total,
+                (long long)workspace_bytes);
+  if (T > 0 && ((uintptr_t)workspace & 255u))
+    return fail(DPPO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+  rocblas_handle blas = nullptr;
+  if ((dhidden || dweight) && T > 0) {
+    if (blas_handle(&blas) != rocblas_status_success)
+      return fail(DPPO_ERR_HIP, "rocBLAS handle creation failed");
+  }
+  hipStream_t st = (hipStream_t)stream;
+  dppo::launch_prep_stats(loss_mask, T, stats_out, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "prep_stats launch");
+  if (T == 0) {
+    if (dweight && (e = dppo::launch_lmh_zero(dweight, V * d, st)) != hipSuccess)
+      return hip_fail(e, "zero fill");
+  } else {
+    char* ws = (char*)workspace;
+    dppo::LmhArgs m{};
+    m.hidden = (const uint16_t*)hidden;
+    m.weight = (const uint16_t*)weight;
+    m.T = (int32_t)T;
+    m.d = (int32_t)d;
+    m.V = (int32_t)V;
+    m.n0 = 0;
+    m.n1 = (int32_t)V;
+    m.part = (float*)(ws + L.part);
+    m.zy = (float*)(ws + L.zy);
+    m.w = (float*)(ws + L.w);
+    m.lse2 = (float*)(ws + L.lse2);
+    m.ev = (uint8_t*)(ws + L.ev);
+    m.ids = token_ids;
+    m.g = (uint16_t*)(ws + L.g);
+    m.ldg = L.ldg;
+    dppo::RowArgs a{};
+    a.ids = token_ids;
+    a.lp_mu = logp_mu_old;
+    a.lp_ref = p->ref_mode == DPPO_REF_GIVEN ? logp_ref : nullptr;
+    a.adv = advantages;
+    a.mask = loss_mask;
+    a.tscale = token_scale;
+    a.lp_out = logp_out;
+    a.loss_tok = loss_tok_out;
+    a.flags = flags_out;
+    a.stats = stats_out;
+    a.T = (int32_t)T;
+    a.V = (int32_t)V;
+    a.mode = dppo::kModeLoss;
+    a.band_lo = p->band_lo;
+    a.band_hi = p->band_hi;
+    a.clip_lo = 1.0f - p->clip_eps_lo;
+    a.clip_hi = 1.0f + p->clip_eps_hi;
+    a.loss_scale = p->loss_scale;
+    a.rd_mode = p->rd_mode;
+    a.scale_mode = p->scale_mode;
+    a.ref_mode = p->ref_mode;
+    a.alpha = p->alpha;
+    if ((e = dppo::launch_lmh_zy(m, st)) != hipSuccess) return hip_fail(e, "z_y launch");
+    auto* ev = timer_slot();
+    if (ev) (void)hipEventRecord(ev->first, st);
+    e = dppo::launch_lmh_fwd_tiles(m, st);
+    if (ev) (void)hipEventRecord(ev->second, st);
+    if (e != hipSuccess) return hip_fail(e, "forward tile launch");
+    if ((e = dppo::launch_lmh_finish(a, m, st)) != hipSuccess) return hip_fail(e, "finish launch");
+    if (dhidden || dweight) {
+      if (rocblas_set_stream(blas, st) != rocblas_status_success)
+        return fail(DPPO_ERR_HIP, "rocblas_set_stream failed");
+      const float one = 1.0f, zero = 0.0f;
+      for (int64_t n0 = 0; n0 < V; n0 += L.chunk) {
+        const int64_t n1 = std::min<int64_t>(V, n0 + L.chunk);
+        m.n0 = (int32_t)n0;
+        m.n1 = (int32_t)n1;
+        auto* evb = timer_slot();
+        if (evb) (void)hipEventRecord(evb->first, st);
+        e = dppo::launch_lmh_bwd_tiles(m, st);
+        if (evb) (void)hipEventRecord(evb->second, st);
+        if (e != hipSuccess) return hip_fail(e, "backward tile launch");
+        const rocblas_int kc = (rocblas_int)(n1 - n0);
+        rocblas_status bs;
+        if (dhidden) {
+          // column-major view: dhidden^T [d x T] (+)= weight_c^T [d x kc] . g^T [kc x T]
+          bs = rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_none,
+                               (rocblas_int)d, (rocblas_int)T, kc, &one,
+                               (const uint16_t*)weight + n0 * d, rocblas_datatype_bf16_r, (rocblas_int)d,
+                               m.g, rocblas_datatype_bf16_r, (rocblas_int)L.ldg,
+                               n0 == 0 ? &zero : &one, dhidden, rocblas_datatype_f32_r, (rocblas_int)d,
+                               dhidden, rocblas_datatype_f32_r, (rocblas_int)d,
+                               rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+          if (bs != rocblas_status_success) return fail(DPPO_ERR_HIP, "rocBLAS dhidden GEMM failed (%d)", (int)bs);
+        }
+        if (dweight) {
+          // column-major view: dweight_c^T [d x kc] = hidden^T [d x T] . g [T x kc]
+          bs = rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_transpose,
+                               (rocblas_int)d, kc, (rocblas_int)T, &one,
+                               hidden, rocblas_datatype_bf16_r, (rocblas_int)d,
+                               m.g, rocblas_datatype_bf16_r, (rocblas_int)L.ldg,
+                               &zero, dweight + n0 * d, rocblas_datatype_f32_r, (rocblas_int)d,
+                               dweight + n0 * d, rocblas_datatype_f32_r, (rocblas_int)d,
+                               rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+          if (bs != rocblas_status_success) return fail(DPPO_ERR_HIP, "rocBLAS dweight GEMM failed (%d)", (int)bs);
+        }
+      }
+    }
   }
   dppo::launch_loss_sum(loss_tok_out, loss_mask, token_scale, stats_out, T, p->loss_scale,
                         p->scale_mode, loss_out, st);

@@ -20,6 +20,10 @@ Workloads (name: what it is):
   large_vocab   T=16384 (32 x 512), V=151936, bf16 logits ~ N(0, 3^2); e_ref ~ N(0, 0.2^2)
                 (staleness drift), e_mu ~ Laplace(0, 0.05) (train-inference discrepancy);
                 A = +-1 per sequence, groups of 8 samples with 4 positive and 4 negative.
+  lm_head       T=8192 (16 x 512), d=4096, V=151936: hidden ~ N(0, 1) and LM-head weight
+                ~ N(0, 0.02^2), both bf16 (logit std about 1.28); noise and advantages as
+                large_vocab. Built by make_lm_head_workload; the logits are formed (chunk by
+                chunk, float32, on the device) only to sample the token ids.
   long_agentic  T=65536 (8 x 8192), V=151936, bf16 logits ~ N(0, 3^2); exactly 40% of
                 positions are tool/observation tokens (mask 0) in alternating spans of mean
                 length 200 (observation) / 300 (assistant); each sequence holds 1-4 policy
@@ -74,6 +78,8 @@ class Workload:
     e_prev: torch.Tensor | None = None   # long_agentic: previous version's extra drift
     segments: np.ndarray | None = None   # long_agentic: per-token staleness gap
     meta: dict = field(default_factory=dict)
+    hidden: torch.Tensor | None = None   # lm_head: [T, d] bf16 (logits is None)
+    weight: torch.Tensor | None = None   # lm_head: [V, d] bf16, the [out, in] layout
 
 
 def _laplace(gen, n, b, device):
@@ -256,3 +262,54 @@ def version_logprobs(anchor: torch.Tensor, wl: Workload):
     prev = lp_old + (wl.e_prev if wl.e_prev is not None else 0.0)
     lp_mu = lp_old + wl.e_mu
     return lp_old.to(torch.float32), prev.to(torch.float32), lp_mu.to(torch.float32)
+
+
+LM_HEAD = dict(n_seq=16, seq_len=512, d=4096, V=151936, seed=4, hidden_std=1.0, weight_std=0.02,
+               ref_std=0.2, mu_laplace=0.05)
+
+
+def make_lm_head_workload(device="cpu", T: int | None = None, d: int | None = None,
+                          V: int | None = None, seed: int | None = None,
+                          seq_len: int | None = None, mask_frac: float = 0.0,
+                          weight_std: float | None = None) -> Workload:
+    """Draw the LM-head workload (hidden states, head weight, ids, noise, advantages)."""
+    cfg = dict(LM_HEAD)
+    seq_len = cfg["seq_len"] if seq_len is None else seq_len
+    T = cfg["n_seq"] * seq_len if T is None else T
+    d = cfg["d"] if d is None else d
+    V = cfg["V"] if V is None else V
+    seed = cfg["seed"] if seed is None else seed
+    wstd = cfg["weight_std"] if weight_std is None else weight_std
+    seq_len = min(seq_len, T) if T > 0 else seq_len
+    n_seq = -(-T // seq_len) if T > 0 else 0
+    device = torch.device(device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    rng = np.random.default_rng(seed)
+    hidden = (cfg["hidden_std"] * torch.randn((T, d), generator=gen, device=device)).to(torch.bfloat16)
+    weight = torch.empty((V, d), dtype=torch.bfloat16, device=device)
+    for a in range(0, V, 8192):                    # draw in float32 slices, store bf16
+        b = min(V, a + 8192)
+        weight[a:b] = (wstd * torch.randn((b - a, d), generator=gen, device=device)).to(torch.bfloat16)
+    ids = torch.empty(T, dtype=torch.int64, device=device)
+    tiny = torch.finfo(torch.float32).tiny
+    for a in range(0, T, 512):                     # Gumbel-max over softmax(hidden weight^T)
+        b = min(T, a + 512)
+        z = hidden[a:b].float() @ weight.float().T if V * d <= (1 << 26) else \
+            torch.cat([hidden[a:b].float() @ weight[c:c + 16384].float().T
+                       for c in range(0, V, 16384)], dim=1)
+        u = torch.rand(z.shape, generator=gen, device=device, dtype=torch.float32)
+        ids[a:b] = torch.argmax(z - torch.log(-torch.log(u.clamp_min(tiny))), dim=1)
+        del z, u
+    if n_seq % 8 == 0 and n_seq > 0:
+        a_seq = _group_pm1_advantages(rng, n_seq)
+    else:
+        a_seq = rng.standard_normal(n_seq)
+    adv = np.repeat(a_seq, seq_len)[:T].astype(np.float32)
+    mask = (rng.random(T) >= mask_frac).astype(np.uint8)
+    e_ref = cfg["ref_std"] * torch.randn(T, generator=gen, device=device, dtype=torch.float64)
+    e_mu = _laplace(gen, T, cfg["mu_laplace"], device)
+    return Workload(name="lm_head", T=T, V=V, seq_len=seq_len, logits=None, ids=ids,
+                    adv=torch.as_tensor(adv, device=device), mask=torch.as_tensor(mask, device=device),
+                    e_ref=e_ref, e_mu=e_mu, meta=dict(cfg, seed=seed, T=T, V=V, d=d),
+                    hidden=hidden, weight=weight)

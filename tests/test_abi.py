@@ -269,3 +269,42 @@ def test_effective_thresholds_reject_bad_arguments(args, frag):
     assert frag in _lib.lib().dppo_last_error().decode()
     assert _lib.lib().dppo_effective_thresholds(0.9, 1.1, 0.8, 1.2, 0.5, 1, None) == \
         _lib.DPPO_ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------------- fused LM head
+def _lmh(T=4, d=64, V=300, dtype=1, hidden=FAKE, weight=FAKE, ws=FAKE, wsb=1 << 40, p=None,
+         loss=FAKE, stats=FAKE):
+    p = p or _params()
+    return _lib.lib().fused_lm_head_loss_fwd_bwd(
+        hidden, weight, dtype, T, d, V, FAKE, FAKE, FAKE, FAKE, None, None, C.byref(p), FAKE,
+        FAKE, loss, None, stats, None, None, 0, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,frag,code", [
+    (dict(dtype=0), "bf16", 2),
+    (dict(dtype=5), "dtype", 1),
+    (dict(d=60), "multiple of 8", 1),
+    (dict(d=0), "multiple of 8", 1),
+    (dict(V=0), "V =", 1),
+    (dict(T=-1), "T =", 1),
+    (dict(hidden=None), "aligned", 1),
+    (dict(weight=FAKE + 8), "aligned", 1),
+    (dict(wsb=100), "workspace", 1),
+    (dict(ws=FAKE + 16), "256-byte", 1),
+    (dict(loss=None), "required", 1),
+    (dict(p=_params(rd_mode=8)), "rd_mode", 1),
+])
+def test_lm_head_rejects_bad_arguments(kw, frag, code):
+    assert _lmh(**kw) == code
+    assert frag in _lib.lib().dppo_last_error().decode()
+
+
+def test_lm_head_workspace_size():
+    L = _lib.lib()
+    T, d, V = 8192, 4096, 151936
+    n = L.fused_lm_head_workspace_bytes(T, d, V, 0)
+    ntiles = -(-V // 128)
+    assert n >= ntiles * T * 8 + T * 13 + T * ntiles * 128 * 2
+    assert L.fused_lm_head_workspace_bytes(T, d, V, 16384) < n
+    assert L.fused_lm_head_workspace_bytes(T, 4, V, 0) == -1
+    assert L.fused_lm_head_workspace_bytes(-1, d, V, 0) == -1

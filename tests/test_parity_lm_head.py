@@ -1,0 +1,181 @@
+"""GPU parity of fused_lm_head_loss_fwd_bwd (through the C ABI) against the float64 oracle.
+
+The oracle forms z = hidden weight^T exactly from the same bf16 bits, runs the loss stage and
+applies the chain rule. Tolerances:
+  * lp, l_t: as the row entry point (bf16 contract 2e-3 relative, floor 1), plus a tight
+    1e-4 bound (fp32 accumulation of d bf16 products);
+  * decisions and stats: exact away from threshold ties;
+  * dhidden, dweight: |gpu - ref| <= 2^-7 (|G| |W|) and 2^-7 (|G|^T |H|) elementwise, where G
+    is the oracle's dlogits: G is rounded to bf16 (2^-9) after an fp32 exponential, and the
+    products accumulate in fp32.
+Every case prints its name and sizes before it touches the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_12070_amd as P
+from paper_2605_12070_amd import workloads as W
+
+from helpers import DELTA, assert_close_rel, bits_of, oracle_params, tie_mask
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _anchor(wl):
+    """Oracle log-probs of the sampled tokens (only to synthesise lp_ref and lp_mu)."""
+    z = bits_of(wl.hidden) @ bits_of(wl.weight).T
+    lp, _ = oracle.logprob_fwd(z, wl.ids.cpu().numpy())
+    return torch.from_numpy(lp)
+
+
+def _grad_bound(G, other):
+    return 2.0 ** -7 * (np.abs(G) @ np.abs(other)) + 1e-7
+
+
+def _run(T, d, V, seed=0, mask_frac=0.2, rd_mode="mask_weight", scale_mode="token_mean",
+         loss_scale=1.0, band=(0.5, 2.0), eps=(0.2, 0.2), ref_mode="given", alpha=0.5,
+         vocab_chunk=0, weight_std=0.1, bad_ids=(), want_grads=True):
+    _say("lm_head", T, d, V, seed, mask_frac, rd_mode, scale_mode, ref_mode, vocab_chunk)
+    wl = W.make_lm_head_workload(DEV, T=T, d=d, V=V, seed=seed, seq_len=8,
+                                 mask_frac=mask_frac, weight_std=weight_std)
+    for t in bad_ids:
+        wl.ids[t] = V + 3 if t % 2 else -1
+    anchor = _anchor(wl)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    if ref_mode == "given":
+        ref_in = lp_ref
+    else:
+        f = oracle.log_linear_proxy_logprob if ref_mode == "log_linear" else oracle.linear_proxy_logprob
+        ref_in = torch.from_numpy(f(lp_mu.cpu().double().numpy(), anchor.numpy(), alpha))
+    res = P.fused_lm_head_loss_fwd_bwd(
+        wl.hidden, wl.weight, wl.ids, lp_mu, lp_ref if ref_mode == "given" else None, wl.adv,
+        wl.mask, band=band, clip_eps=eps, rd_mode=rd_mode, scale_mode=scale_mode,
+        loss_scale=loss_scale, ref_mode=ref_mode, alpha=alpha, vocab_chunk=vocab_chunk,
+        want_grads=want_grads)
+    torch.cuda.synchronize()
+    params = oracle_params(band, eps, rd_mode, scale_mode, loss_scale)
+    H, Wt = bits_of(wl.hidden), bits_of(wl.weight)
+    ref = oracle.lm_head_loss(H, Wt, wl.ids.cpu().numpy(), lp_mu.cpu().double().numpy(),
+                              ref_in.cpu().double().numpy(), wl.adv.cpu().double().numpy(),
+                              wl.mask.cpu().numpy(), None, params, want_grads=want_grads)
+    ties = tie_mask(ref, params)
+    lp = res.logp.cpu().double().numpy()
+    assert_close_rel(lp, ref["lp"], 2e-3, "lp")
+    assert_close_rel(lp, ref["lp"], 1e-4, "lp (tight)")
+    lt = res.loss_tok.cpu().double().numpy()
+    assert_close_rel(lt, ref["loss_tok"], 1e-4, "loss_tok", mask=~ties)
+    fl = res.flags.cpu().numpy()
+    assert np.array_equal(fl[~ties], ref["flags"][~ties]), "flags differ away from ties"
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
+    if ties.sum() == 0:
+        np.testing.assert_array_equal(st, ref["stats"])
+        denom = np.nansum(np.abs(np.where(ref["valid"], ref["s"] * ref["loss_tok"], 0.0))) + 1e-30
+        assert abs(res.loss.item() - ref["loss"]) <= 1e-5 * denom
+    if want_grads:
+        G = ref["dlogits"].copy()
+        G[ties] = 0.0                      # tie rows may take either decision: excluded below
+        keep = ~ties
+        dh = res.dhidden.cpu().double().numpy()
+        bound = _grad_bound(G, Wt)
+        err = np.abs(dh - ref["dhidden"])
+        assert np.all(err[keep] <= bound[keep]), f"dhidden: worst excess {np.max(err[keep] - bound[keep]):.3e}"
+        if ties.sum() == 0:
+            dw = res.dweight.cpu().double().numpy()
+            bound = _grad_bound(G.T, H)
+            err = np.abs(dw - ref["dweight"])
+            assert np.all(err <= bound), f"dweight: worst excess {np.max(err - bound):.3e}"
+    else:
+        assert res.dhidden is None and res.dweight is None
+    _say("lm_head ok", "ties", int(ties.sum()))
+    return wl, res, ref
+
+
+@pytest.mark.parametrize("rd_mode", ["none", "mask", "weight", "mask_weight"])
+def test_small_ragged(rd_mode):
+    # T and V not multiples of the 128 x 128 tile; d not a multiple of the 64-wide K step
+    _run(200, 200, 1000, seed=1, rd_mode=rd_mode, bad_ids=(3, 4))
+
+
+def test_const_scale_and_unit_loss():
+    _run(130, 256, 640, seed=2, scale_mode="const", loss_scale=1.0, mask_frac=0.0)
+
+
+def test_vocab_chunks():
+    # backward in vocabulary chunks of 256 rows (5 chunks, the last ragged)
+    _run(256, 128, 1100, seed=3, vocab_chunk=256)
+
+
+@pytest.mark.parametrize("kind", ["log_linear", "linear"])
+def test_interpolated_reference(kind):
+    _run(128, 128, 512, seed=4, ref_mode=kind, alpha=0.5, band=(0.99, 1.01), eps=(0.003, 0.004))
+
+
+def test_forward_only():
+    _run(96, 64, 300, seed=5, want_grads=False)
+
+
+def test_single_token_single_tile():
+    _run(1, 8, 5, seed=6, mask_frac=0.0)
+
+
+def test_empty_batch():
+    _say("lm_head empty")
+    h = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
+    w = torch.randn(300, 64, device=DEV).to(torch.bfloat16)
+    e = torch.zeros(0, device=DEV)
+    res = P.fused_lm_head_loss_fwd_bwd(h, w, torch.zeros(0, dtype=torch.int64, device=DEV), e, e, e)
+    torch.cuda.synchronize()
+    assert res.loss.item() == 0.0 and res.stats.sum().item() == 0
+    assert res.dweight.abs().sum().item() == 0.0
+
+
+def test_lm_head_workload_sampled_rows():
+    """The full-size LM-head workload (T = 8192, d = 4096, V = 151936): sampled rows of lp,
+    loss and dhidden against the oracle's row-level computation on z_t = hidden_t weight^T,
+    and the property that dweight's columns sum to zero over the vocabulary (each G row sums
+    to zero)."""
+    _say("lm_head full size")
+    wl = W.make_lm_head_workload(DEV)
+    T, V = wl.T, wl.V
+    z_rows = None
+    lp_anchor = torch.empty(T, dtype=torch.float64)
+    # anchor from a float32 torch pass (input synthesis only)
+    for a in range(0, T, 512):
+        z = wl.hidden[a:a + 512].float() @ wl.weight.float().T
+        lse = torch.logsumexp(z, dim=1)
+        lp_anchor[a:a + 512] = (z.gather(1, wl.ids[a:a + 512, None])[:, 0] - lse).double().cpu()
+        del z
+    lp_ref, lp_mu = W.reference_logprobs(lp_anchor, wl)
+    res = P.fused_lm_head_loss_fwd_bwd(wl.hidden, wl.weight, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(0).choice(T, size=6, replace=False))
+    Wt = bits_of(wl.weight)
+    H = bits_of(wl.hidden[torch.as_tensor(rows, device=DEV)])
+    z_rows = H @ Wt.T
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    scale = oracle.batch_scale(wl.mask.cpu().numpy(), params)
+    ref = oracle.per_token(z_rows, wl.ids.cpu().numpy()[rows], lp_mu.cpu().double().numpy()[rows],
+                           lp_ref.cpu().double().numpy()[rows], wl.adv.cpu().double().numpy()[rows],
+                           wl.mask.cpu().numpy()[rows], None, params, scale, want_dlogits=True)
+    lp = res.logp.cpu().double().numpy()[rows]
+    assert_close_rel(lp, ref["lp"], 1e-4, "lp")
+    dh_ref = ref["dlogits"] @ Wt
+    dh = res.dhidden[torch.as_tensor(rows, device=DEV)].cpu().double().numpy()
+    bound = _grad_bound(ref["dlogits"], Wt)
+    assert np.all(np.abs(dh - dh_ref) <= bound)
+    # sum_v dweight[v] = sum_t (sum_v G[t, v]) hidden_t and every G row sums to zero; the
+    # bf16 rounding of G leaves at most 2^-8 sum_v |G[t, v]| <= 2^-8 * 2 |w_t| per row, with
+    # |w_t| <= s wd r_s |A| <= (1 / n_valid) * 2 * 1.2 * 1 here (band [0.5, 2], clip 0.2)
+    col = res.dweight.double().sum(dim=0).cpu().numpy()
+    n_valid = int(wl.mask.sum().item())
+    habs = wl.hidden.float().abs().double().sum(dim=0).cpu().numpy()
+    assert np.all(np.abs(col) <= 2.0 ** -7 * (4.8 / n_valid) * habs + 1e-9)
+    _say("lm_head full size ok", res.stats.cpu().numpy().tolist())
