@@ -9,11 +9,16 @@
 
 namespace dppo {
 
-// Macro tile of the GEMM kernels: LMH_BM tokens x LMH_BN vocabulary rows, K in steps of
-// LMH_BK hidden features.
-constexpr int LMH_BM = 128;
-constexpr int LMH_BN = 128;
+// Tile of the GEMM kernels: LMH_WM x LMH_WN waves, each with LMH_TM x LMH_TN matrix-core
+// tiles of 32 x 32, so a workgroup of LMH_THREADS threads covers LMH_BM tokens x LMH_BN
+// vocabulary rows; K advances LMH_BK hidden features per LDS stage.
+constexpr int LMH_WM = 2, LMH_WN = 4;
+constexpr int LMH_TM = 4, LMH_TN = 2;
+constexpr int LMH_BM = 32 * LMH_WM * LMH_TM;
+constexpr int LMH_BN = 32 * LMH_WN * LMH_TN;
 constexpr int LMH_BK = 64;
+constexpr int LMH_THREADS = 64 * LMH_WM * LMH_WN;
+constexpr int LMH_STAGES = 2;
 
 struct LmhArgs {
   const uint16_t* hidden;  // [T, d] bf16, rows contiguous

@@ -19,76 +19,77 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-// Tile engine. 256 threads = 4 waves in a 2 x 2 arrangement; wave (wm, wn) owns TM x TN
-// MFMA tiles of 32 x 32, so the workgroup tile is (64 TM) tokens x (64 TN) vocabulary rows.
-// K advances LMH_BK at a time through two LDS stages (rows padded by 8 bf16 so that the 16-byte
-// fragment reads of 16 lanes hit distinct banks); the next stage's global loads are in
-// flight while the current stage is multiplied.
-template <int TM, int TN>
-struct Cfg {
-  static constexpr int BM = 64 * TM, BN = 64 * TN, BK = LMH_BK, LDK = BK + 8;
-  static constexpr int KC = BK / 8;                     // 16-byte chunks per tile row
-  static constexpr int A_EL = BM * LDK, B_EL = BN * LDK;
-  static constexpr int STAGE = (A_EL + B_EL) * 2;       // bytes of one stage (A and B)
-  static constexpr int CA = BM * BK / 8 / 256;          // 16-byte chunks per thread, A
-  static constexpr int CB = BN * BK / 8 / 256;          // and B
-  static constexpr int LDC = BN + 4;                    // staged C row (fp32)
-  static constexpr int STG = 64 * LDC * 4;              // one pass: 64 token rows
-  static constexpr int SMEM = 2 * STAGE > STG ? 2 * STAGE : STG;
-};
-using LC = Cfg<LMH_BM / 64, LMH_BN / 64>;
-static_assert(LC::BM == LMH_BM && LC::BN == LMH_BN && LC::BK == LMH_BK, "tile constants");
+// Tile engine: hidden[m0 : m0 + BM] . weight[r0 : r0 + BN]^T on the matrix cores, fed by
+// buffer-to-LDS loads (gfx950 writes lane l's 16 bytes at the wave's LDS base + 16 l, and
+// zeros for a lane whose offset lies outside the resource, which bounds every access to
+// the tile's rows and turns a K tail past d into zeros). There is no register staging:
+// LMH_STAGES LDS stages form a ring, and the loads of stage k + LMH_STAGES - 1 are issued
+// while stage k is multiplied. A stage holds the A and B tiles as 128-byte rows (64 bf16 of
+// K); the 16-byte chunk c of row r sits at position c ^ ((r / 2) % 8), so the fragment
+// reads of 16 lanes (16 consecutive rows, one chunk) cover all 64 banks. Each stage is its
+// own LDS object, which lets the compiler track the loads into each separately.
+// Wave (wm, wn) owns TM x TN tiles of 32 x 32 (v_mfma_f32_32x32x16_bf16, fp32 accumulation;
+// operand lane l holds row l % 32, K 8 (l / 32) .. +7). After the K loop, epi(Cs, mi, ldc)
+// runs in TM passes; pass mi stages, for every wave row wm, the 32 token rows
+// wm * 32 TM + mi * 32 + [0, 32) as Cs[s][col], s = wm * 32 + row % 32, col in [0, BN).
+constexpr int kWaves = LMH_WM * LMH_WN;
+constexpr int kIA = LMH_BM / 8 / kWaves;        // loads per wave and stage, A (8 rows each)
+constexpr int kIB = LMH_BN / 8 / kWaves;        // and B
+constexpr int kAEl = LMH_BM * LMH_BK;           // bf16 elements of the A tile (B follows)
+constexpr int kStageEl = (LMH_BM + LMH_BN) * LMH_BK;
+constexpr int kRows = 32 * LMH_WM;              // staged rows per epilogue pass
+constexpr int kLdc = LMH_BN + 8;                // staged row stride (floats): rows 8 apart
+                                                // in bank, so 8 rows x 8 lanes are distinct
+static_assert(LMH_BK == 64 && LMH_BM % (8 * kWaves) == 0 && LMH_BN % (8 * kWaves) == 0,
+              "tile shape");
+static_assert(kRows * kLdc * 4 <= LMH_STAGES * kStageEl * 2, "an epilogue pass fits in the ring");
+static_assert(LMH_STAGES >= 2 && LMH_STAGES <= 4, "ring depth");
 
-// Computes the tile hidden[m0 : m0 + BM] . weight[r0 : r0 + BN]^T (rows past T or V read as
-// zeros through the buffer range checks; a K tail past d reads zeros through an offset
-// outside the resource), then hands it to epi(Cs, mi) in TM passes: pass mi stages, for
-// both wave rows wm, the 32 token rows wm * 32 TM + mi * 32 + [0, 32) as Cs[s][col] with
-// s = wm * 32 + row % 32 and col in [0, BN).
-template <int TM, int TN, typename Epi>
-__device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0, char* smem, Epi&& epi) {
-  using C = Cfg<TM, TN>;
+template <typename Epi>
+__device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
+                                           uint16_t* (&st)[LMH_STAGES], Epi&& epi) {
+  constexpr int TM = LMH_TM, TN = LMH_TN, BK = LMH_BK;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / LMH_WN, wn = wave % LMH_WN;
   const int d = m.d;
-  const int rows_a = min(C::BM, m.T - m0);
-  const int rows_b = min(C::BN, m.V - r0);
+  const int rows_a = min(LMH_BM, m.T - m0);
+  const int rows_b = min(LMH_BN, m.V - r0);
   const __amdgpu_buffer_rsrc_t ra = row_rsrc(m.hidden + (int64_t)m0 * d, rows_a * d * 2);
   const __amdgpu_buffer_rsrc_t rb = row_rsrc(m.weight + (int64_t)r0 * d, rows_b * d * 2);
 
-  // chunk c = tid + 256 i of a tile is row c / KC, columns 8 (c % KC) .. +7
-  int ga_off[C::CA], la_off[C::CA], gb_off[C::CB], lb_off[C::CB];
-  int kcol_a[C::CA], kcol_b[C::CB];
+  // Load i of wave w covers tile rows 8 (w I + i) .. +7: lane l takes row 8 (w I + i) + l / 8
+  // at position l % 8, i.e. K chunk (l % 8) ^ ((row / 2) % 8).
+  int goa[kIA], gob[kIB];
 #pragma unroll
-  for (int i = 0; i < C::CA; ++i) {
-    const int c = tid + 256 * i, row = c / C::KC, kc = (c % C::KC) * 8;
-    kcol_a[i] = kc;
-    ga_off[i] = (row * d + kc) * 2;
-    la_off[i] = row * C::LDK + kc;
+  for (int i = 0; i < kIA; ++i) {
+    const int row = 8 * (wave * kIA + i) + (lane >> 3);
+    goa[i] = (row * d + ((lane & 7) ^ ((row >> 1) & 7)) * 8) * 2;
   }
 #pragma unroll
-  for (int i = 0; i < C::CB; ++i) {
-    const int c = tid + 256 * i, row = c / C::KC, kc = (c % C::KC) * 8;
-    kcol_b[i] = kc;
-    gb_off[i] = (row * d + kc) * 2;
-    lb_off[i] = C::A_EL + row * C::LDK + kc;
+  for (int i = 0; i < kIB; ++i) {
+    const int row = 8 * (wave * kIB + i) + (lane >> 3);
+    gob[i] = (row * d + ((lane & 7) ^ ((row >> 1) & 7)) * 8) * 2;
   }
-  u32x4 ga[C::CA], gb[C::CB];
-  auto gload = [&](int k0) {
+  auto issue = [&](uint16_t* s, int kb) {
+    const int k0 = kb * BK;
 #pragma unroll
-    for (int i = 0; i < C::CA; ++i)
-      ga[i] = buf_load16(ra, (k0 + kcol_a[i] < d) ? ga_off[i] + k0 * 2 : 0x7fffff00, 0);
+    for (int i = 0; i < kIA; ++i) {
+      const int row = 8 * (wave * kIA + i) + (lane >> 3);
+      const int kc = (lane & 7) ^ ((row >> 1) & 7);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ra, (__attribute__((address_space(3))) void*)(s + (wave * kIA + i) * 512), 16,
+          (k0 + kc * 8 < d) ? goa[i] + k0 * 2 : 0x7fffff00, 0, 0, 0);
+    }
 #pragma unroll
-    for (int i = 0; i < C::CB; ++i)
-      gb[i] = buf_load16(rb, (k0 + kcol_b[i] < d) ? gb_off[i] + k0 * 2 : 0x7fffff00, 0);
-  };
-  auto lstore = [&](int stage) {
-    uint16_t* S = (uint16_t*)(smem + stage * C::STAGE);
-#pragma unroll
-    for (int i = 0; i < C::CA; ++i) *(u32x4*)(S + la_off[i]) = ga[i];
-#pragma unroll
-    for (int i = 0; i < C::CB; ++i) *(u32x4*)(S + lb_off[i]) = gb[i];
+    for (int i = 0; i < kIB; ++i) {
+      const int row = 8 * (wave * kIB + i) + (lane >> 3);
+      const int kc = (lane & 7) ^ ((row >> 1) & 7);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (__attribute__((address_space(3))) void*)(s + kAEl + (wave * kIB + i) * 512), 16,
+          (k0 + kc * 8 < d) ? gob[i] + k0 * 2 : 0x7fffff00, 0, 0, 0);
+    }
   };
 
   f32x16 acc[TM][TN];
@@ -99,39 +100,81 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0, cha
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
 
-  const int nk = (d + C::BK - 1) / C::BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kb = 0; kb < nk; ++kb) {
-    const int cur = kb & 1;
-    if (kb + 1 < nk) gload((kb + 1) * C::BK);
-    const uint16_t* As = (const uint16_t*)(smem + cur * C::STAGE);
-    const uint16_t* Bs = As + C::A_EL;
+  // Fragment reads run one K step ahead of the matrix-core instructions that use them.
+  auto frags = [&](const uint16_t* s, int ks, bf16x8 (&af)[TM], bf16x8 (&bfr)[TN]) {
+    const int kc = 2 * ks + (lane >> 5);
 #pragma unroll
-    for (int ks = 0; ks < C::BK / 16; ++ks) {
-      // 32x32x16 operands: lane l holds row (l % 32), k = 8 (l / 32) .. +7
-      const int kk = ks * 16 + 8 * (lane >> 5);
-      bf16x8 af[TM], bfr[TN];
+    for (int mi = 0; mi < TM; ++mi) {
+      const int R = wm * 32 * TM + mi * 32 + (lane & 31);
+      af[mi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + R * BK + ((kc ^ ((R >> 1) & 7)) * 8)));
+    }
 #pragma unroll
-      for (int mi = 0; mi < TM; ++mi)
-        af[mi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(As + (wm * 32 * TM + mi * 32 + (lane & 31)) * C::LDK + kk));
+    for (int ni = 0; ni < TN; ++ni) {
+      const int R = wn * 32 * TN + ni * 32 + (lane & 31);
+      bfr[ni] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + kAEl + R * BK + ((kc ^ ((R >> 1) & 7)) * 8)));
+    }
+  };
+  auto compute = [&](const uint16_t* s) {
+    bf16x8 a0[TM], b0[TN], a1[TM], b1[TN];
+    frags(s, 0, a0, b0);
 #pragma unroll
-      for (int ni = 0; ni < TN; ++ni)
-        bfr[ni] = __builtin_bit_cast(bf16x8, *(const u32x4*)(Bs + (wn * 32 * TN + ni * 32 + (lane & 31)) * C::LDK + kk));
+    for (int ks = 0; ks < BK / 16; ks += 2) {
+      frags(s, ks + 1, a1, b1);
+      __builtin_amdgcn_sched_barrier(0);       // keep the reads ahead of the MFMAs
 #pragma unroll
       for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mi], b0[ni], acc[mi][ni], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ks + 2 < BK / 16) frags(s, ks + 2, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mi], b1[ni], acc[mi][ni], 0, 0, 0);
     }
-    if (kb + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
+  };
+  // Barrier without a memory fence (a fence would wait for the loads still in flight); the
+  // empty asm statements keep the compiler from moving memory accesses across it.
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  constexpr int S = LMH_STAGES;
+  const int nk = (d + BK - 1) / BK;
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(st[s], s);
+  for (int kb0 = 0; kb0 < nk; kb0 += S) {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const int kb = kb0 + j;
+      if (kb < nk) {
+        // This wave's loads of stage kb are complete once at most the loads of the S - 2
+        // later stages are outstanding; after the barrier, every wave's are.
+        if (kb + S - 2 < nk) {
+          if constexpr (S == 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          if constexpr (S == 3) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kIA + kIB) : "memory");
+          if constexpr (S == 4) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * (kIA + kIB)) : "memory");
+        } else {
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        barrier();
+        if (kb + S - 1 < nk) issue(st[(j + S - 1) % S], kb + S - 1);
+        compute(st[j]);
+      }
+    }
   }
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+  barrier();
 
   // 32x32 accumulator layout: register r of lane l is row 8 (r / 4) + 4 (l / 32) + r % 4,
-  // column l % 32.
-  float* Cs = (float*)smem;
+  // column l % 32. The passes stage through the ring (its stages are contiguous).
+  float* Cs = (float*)st[0];
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
 #pragma unroll
@@ -140,57 +183,67 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0, cha
       for (int r = 0; r < 16; ++r) {
         const int s = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         const int col = wn * 32 * TN + ni * 32 + (lane & 31);
-        Cs[s * C::LDC + col] = acc[mi][ni][r];
+        Cs[s * kLdc + col] = acc[mi][ni][r];
       }
     __syncthreads();
-    epi((const float*)Cs, mi);
+    epi((const float*)Cs, mi, kLdc);
     __syncthreads();
   }
 }
 
 // Token row of staged row s in pass mi.
 __device__ __forceinline__ int lmh_token(int m0, int s, int mi) {
-  return m0 + (s >> 5) * 32 * (LMH_BM / 64) + mi * 32 + (s & 31);
+  return m0 + (s >> 5) * 32 * LMH_TM + mi * 32 + (s & 31);
 }
 
 }  // namespace
 
+#define LMH_RUN_ENGINE(m, m0, r0, epi)                                                    \
+  do {                                                                                    \
+    __shared__ __align__(16) uint16_t lmh_st[LMH_STAGES][kStageEl];                       \
+    uint16_t* ring[LMH_STAGES];                                                           \
+    _Pragma("unroll") for (int i = 0; i < LMH_STAGES; ++i) ring[i] = lmh_st[i];            \
+    lmh_engine(m, m0, r0, ring, epi);                                                     \
+  } while (0)
+
 // Forward: per-token partial log-sum-exp (log2 domain) of one LMH_BN-entry vocabulary tile.
 // An entry of z that is NaN or +inf makes the partial sum NaN; a tile of only -inf logits
 // contributes nothing.
-__global__ __launch_bounds__(256) void lmh_fwd_tiles(LmhArgs m) {
-  __shared__ __align__(16) char smem[LC::SMEM];
+__global__ __launch_bounds__(LMH_THREADS) void lmh_fwd_tiles(LmhArgs m) {
   const int m0 = blockIdx.x * LMH_BM;
   const int nt = blockIdx.y;
   const int r0 = m.n0 + nt * LMH_BN;
   const int ncols = min(LMH_BN, m.n1 - r0);
   const int tid = threadIdx.x;
-  const int s = tid >> 2, q = tid & 3;          // 4 threads per staged row
-  constexpr int QC = LMH_BN / 4;                // columns per thread
-  lmh_engine<LMH_BM / 64, LMH_BN / 64>(m, m0, r0, smem, [&](const float* Cs, int mi) {
-    const float* cr = Cs + s * LC::LDC + q * QC;
-    const int lim = ncols - q * QC;              // valid columns of this quarter
+  constexpr int TPR = LMH_THREADS / kRows;      // threads per staged row
+  constexpr int QC = LMH_BN / TPR;              // columns per thread
+  const int s = tid / TPR, q = tid % TPR;
+  auto epi = [&](const float* Cs, int mi, int ldc) {
+    // thread q of a row takes columns q, q + TPR, q + 2 TPR, ...: the TPR threads of a row
+    // read consecutive words, and the padded stride puts the rows of a wave in other banks
+    const float* cr = Cs + s * ldc + q;
     float mx = -INFINITY;
 #pragma unroll 16
     for (int j = 0; j < QC; ++j)
-      if (j < lim) mx = fmaxf(mx, cr[j]);
+      if (j * TPR + q < ncols) mx = fmaxf(mx, cr[j * TPR]);
     const float m2 = mx * kLog2e;
     float sum = 0.0f;
     if (mx != -INFINITY) {
 #pragma unroll 16
       for (int j = 0; j < QC; ++j)
-        if (j < lim) sum += exp2_hw(__builtin_fmaf(cr[j], kLog2e, -m2));
+        if (j * TPR + q < ncols) sum += exp2_hw(__builtin_fmaf(cr[j * TPR], kLog2e, -m2));
     }
     float n = (mx == -INFINITY) ? -INFINITY : m2;
-    merge_ns(n, sum, __shfl_xor(n, 1, 64), __shfl_xor(sum, 1, 64));
-    merge_ns(n, sum, __shfl_xor(n, 2, 64), __shfl_xor(sum, 2, 64));
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) merge_ns(n, sum, __shfl_xor(n, o, 64), __shfl_xor(sum, o, 64));
     const int t = lmh_token(m0, s, mi);
     if (q == 0 && t < m.T) {
       float* p = m.part + ((int64_t)nt * m.T + t) * 2;
       p[0] = n;
       p[1] = sum;
     }
-  });
+  };
+  LMH_RUN_ENGINE(m, m0, r0, epi);
 }
 
 // z[t, y_t] = hidden[t] . weight[y_t]: one wave per token, fp32 accumulation.
@@ -273,43 +326,43 @@ __global__ __launch_bounds__(256) void lmh_finish(RowArgs a, LmhArgs m) {
 
 // Backward: g[t, v - n0] = w_t (softmax(z_t)[v] - 1{v = y_t}) in bf16 for the tile's rows
 // of the chunk [n0, n1); tokens that were not evaluated get zeros.
-__global__ __launch_bounds__(256) void lmh_bwd_tiles(LmhArgs m) {
-  __shared__ __align__(16) char smem[LC::SMEM];
+__global__ __launch_bounds__(LMH_THREADS) void lmh_bwd_tiles(LmhArgs m) {
   const int m0 = blockIdx.x * LMH_BM;
   const int r0 = m.n0 + blockIdx.y * LMH_BN;
   const int ncols = min(LMH_BN, m.n1 - r0);
-  constexpr int SEGS = LMH_BN / 8;              // 8-column segments of a staged row
-  lmh_engine<LMH_BM / 64, LMH_BN / 64>(m, m0, r0, smem, [&](const float* Cs, int mi) {
+  constexpr int GRP = LMH_BN / 4;                // 4-column groups of a staged row
+  auto epi = [&](const float* Cs, int mi, int ldc) {
+    // a wave covers 64 consecutive 4-column groups of one row: its 16-byte reads of 16
+    // lanes hit 64 distinct banks, and its 8-byte stores are contiguous
 #pragma unroll 2
-    for (int i = 0; i < 64 * SEGS / 256; ++i) {
-      const int idx = threadIdx.x + 256 * i;
-      const int s = idx / SEGS, c0 = (idx % SEGS) * 8;
+    for (int i = 0; i < kRows * GRP / LMH_THREADS; ++i) {
+      const int idx = threadIdx.x + LMH_THREADS * i;
+      const int s = idx / GRP, c0 = (idx % GRP) * 4;
       const int t = lmh_token(m0, s, mi);
       if (t >= m.T || c0 >= ncols) continue;
       const bool ev = m.ev[t] != 0;
       const float wt = m.w[t], l2 = m.lse2[t];
       const int64_t y = m.ids[t];
-      const float* cr = Cs + s * LC::LDC + c0;
-      float o[8];
+      const f32x4 x = *(const f32x4*)(Cs + s * ldc + c0);
+      float o[4];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float p = exp2_hw(__builtin_fmaf(cr[j], kLog2e, -l2));
+      for (int j = 0; j < 4; ++j) {
+        const float p = exp2_hw(__builtin_fmaf(x[j], kLog2e, -l2));
         const float oh = (int64_t)(r0 + c0 + j) == y ? 1.0f : 0.0f;
         o[j] = ev ? wt * (p - oh) : 0.0f;
       }
       uint16_t* dst = m.g + (int64_t)t * m.ldg + (r0 - m.n0) + c0;
-      if (c0 + 8 <= ncols) {
-        u32x4 v;
+      if (c0 + 4 <= ncols) {
+        u32x2 v;
         v.x = pack_bf16(o[0], o[1]);
         v.y = pack_bf16(o[2], o[3]);
-        v.z = pack_bf16(o[4], o[5]);
-        v.w = pack_bf16(o[6], o[7]);
-        *(u32x4*)dst = v;
+        *(u32x2*)dst = v;
       } else {
         for (int j = 0; j < ncols - c0; ++j) dst[j] = to_bf16(o[j]);
       }
     }
-  });
+  };
+  LMH_RUN_ENGINE(m, m0, r0, epi);
 }
 
 hipError_t launch_lmh_zy(const LmhArgs& m, hipStream_t st) {
@@ -319,7 +372,7 @@ hipError_t launch_lmh_zy(const LmhArgs& m, hipStream_t st) {
 
 hipError_t launch_lmh_fwd_tiles(const LmhArgs& m, hipStream_t st) {
   const dim3 grid((m.T + LMH_BM - 1) / LMH_BM, lmh_tiles(m.n1 - m.n0));
-  lmh_fwd_tiles<<<grid, 256, 0, st>>>(m);
+  lmh_fwd_tiles<<<grid, LMH_THREADS, 0, st>>>(m);
   return hipGetLastError();
 }
 
@@ -330,7 +383,7 @@ hipError_t launch_lmh_finish(const RowArgs& a, const LmhArgs& m, hipStream_t st)
 
 hipError_t launch_lmh_bwd_tiles(const LmhArgs& m, hipStream_t st) {
   const dim3 grid((m.T + LMH_BM - 1) / LMH_BM, lmh_tiles(m.n1 - m.n0));
-  lmh_bwd_tiles<<<grid, 256, 0, st>>>(m);
+  lmh_bwd_tiles<<<grid, LMH_THREADS, 0, st>>>(m);
   return hipGetLastError();
 }
 
