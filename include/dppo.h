@@ -129,6 +129,27 @@ dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V,
                         const int64_t* token_ids, float* logp_out, float* lse_out,
                         void* stream);
 
+/* Most policy versions one logprob_fwd_versioned call can read. */
+#define DPPO_MAX_VERSIONS 8
+
+/*
+ * logprob_fwd_versioned -- logprob_fwd for a batch whose tokens were generated by different
+ * policy versions (partial rollouts): token t's log-prob is read from the logits of the
+ * version that produced it, version_ids[t]. These are the exact old log-probs of the
+ * snapshot route (Sec. 5.1): one forward pass per stored version, then the per-token
+ * log-prob under the right one.
+ *
+ *  logits       host array of K device pointers; logits[v] is version v's [T, ld] matrix of
+ *               `dtype` (all K share dtype, T, V and ld). 1 <= K <= DPPO_MAX_VERSIONS.
+ *  version_ids  [T] int32 device array. A token whose version lies outside [0, K) gets
+ *               log-prob NaN (like an out-of-range token id).
+ *  Other arguments as logprob_fwd. Only the selected version's row of each token is read.
+ */
+dppo_status logprob_fwd_versioned(const void* const* logits, int32_t K, int32_t dtype, int64_t T,
+                                  int64_t V, int64_t ld, const int32_t* version_ids,
+                                  const int64_t* token_ids, float* logp_out, float* lse_out,
+                                  void* stream);
+
 /*
  * decoupled_ppo_loss_fwd_bwd -- the fused loss stage: log-prob through a vocabulary-wide
  * log-sum-exp, ratios r_s = pi_theta / pi_ref and r_d = pi_ref / mu_old (Eq. 1, Sec. 3.2),

@@ -462,3 +462,19 @@ def lm_head_loss(hidden, weight, ids, lp_mu, lp_ref, adv, mask=None, token_scale
         out["dhidden"] = g @ wt
         out["dweight"] = g.T @ h
     return out
+
+
+def versioned_logprob(logits_by_version, version, ids):
+    """Exact old log-probs of a partial rollout (Sec. 5.1, snapshot route): token t's
+    log-prob under the policy version that generated it, log pi_{v_t}(y_t), with v_t =
+    version[t]; NaN where v_t is not one of the given versions (or y_t is out of range)."""
+    version = np.asarray(version)
+    ids = np.asarray(ids)
+    T = ids.shape[0]
+    out = np.full(T, np.nan)
+    for v, z in enumerate(logits_by_version):
+        rows = np.nonzero(version == v)[0]
+        if rows.size:
+            lp, _ = logprob_fwd(as_f64(np.asarray(z)[rows]), ids[rows])
+            out[rows] = lp
+    return out

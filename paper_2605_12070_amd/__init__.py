@@ -25,6 +25,7 @@ __all__ = [
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
     "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
     "fused_lm_head_loss_fwd_bwd", "LmHeadResult", "lm_head_workspace_bytes",
+    "logprob_fwd_versioned",
 ]
 
 
@@ -71,6 +72,30 @@ def logprob_fwd(logits: torch.Tensor, token_ids: torch.Tensor, with_lse: bool = 
     st = _lib.lib().logprob_fwd(ptr, _dtype_code(logits), T, V, ld, ids, lp.data_ptr(),
                                 lse.data_ptr() if lse is not None else None, _stream(dev))
     _lib.check(st, "logprob_fwd")
+    return (lp, lse) if with_lse else lp
+
+
+def logprob_fwd_versioned(logits_by_version, version_ids: torch.Tensor, token_ids: torch.Tensor,
+                          with_lse: bool = False):
+    """log pi_{v_t}(y_t) for tokens produced by different policy versions: token t reads row t
+    of logits_by_version[version_ids[t]] (exact old log-probs of a partial rollout)."""
+    mats = list(logits_by_version)
+    if not mats or len(mats) > _lib.MAX_VERSIONS:
+        raise ValueError(f"between 1 and {_lib.MAX_VERSIONS} versions")
+    infos = [_matrix(z, f"logits[{i}]") for i, z in enumerate(mats)]
+    _, T, V, ld = infos[0]
+    if any(i[1:] != (T, V, ld) for i in infos) or any(z.dtype != mats[0].dtype for z in mats):
+        raise ValueError("all versions must share dtype, shape and row stride")
+    dev = mats[0].device
+    ver = _vec(version_ids, T, torch.int32, "version_ids", dev)
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    lp = torch.empty(T, dtype=torch.float32, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev) if with_lse else None
+    arr = (C.c_void_p * len(mats))(*[i[0] for i in infos])
+    st = _lib.lib().logprob_fwd_versioned(arr, len(mats), _dtype_code(mats[0]), T, V, ld, ver, ids,
+                                          lp.data_ptr(), lse.data_ptr() if lse is not None else None,
+                                          _stream(dev))
+    _lib.check(st, "logprob_fwd_versioned")
     return (lp, lse) if with_lse else lp
 
 

@@ -19,6 +19,7 @@ REF_MODES = {"given": 0, "log_linear": 1, "linear": 2}
 FLAG_VALID, FLAG_BAND, FLAG_PPO, FLAG_BAD_ID = 1, 2, 4, 8
 STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
+MAX_VERSIONS = 8
 DTYPE_F32, DTYPE_BF16 = 0, 1
 ABI_VERSION = 2
 
@@ -49,6 +50,7 @@ SIGNATURES = {
                                          C.POINTER(DppoParams), VP, VP, VP, VP, VP, VP, VP,
                                          I64, VP, I64, VP]),
     "fused_lm_head_workspace_bytes": (I64, [I64, I64, I64, I64]),
+    "logprob_fwd_versioned": (I32, [C.POINTER(VP), I32, I32, I64, I64, I64, VP, VP, VP, VP, VP]),
     "dppo_effective_thresholds": (I32, [C.c_double, C.c_double, C.c_double, C.c_double,
                                         C.c_double, I32, C.POINTER(C.c_double)]),
 }

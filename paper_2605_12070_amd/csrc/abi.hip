@@ -103,7 +103,7 @@ hipError_t resident_slots(const dppo::RowLaunch& L, int64_t* slots) {
   return hipSuccess;
 }
 
-dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgs& args, int64_t T,
+dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgsV& args, int64_t T,
                         hipStream_t st) {
   int64_t grid = T;
   if (L.persistent) {
@@ -118,7 +118,9 @@ dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgs& args, int
   }
   auto* ev = timer_slot();
   if (ev) (void)hipEventRecord(ev->first, st);
-  void* kargs[] = {(void*)&args};
+  // Gradient kernels take the RowArgs part alone, the others the whole RowArgsV.
+  const void* karg = L.bwd ? (const void*)static_cast<const dppo::RowArgs*>(&args) : (const void*)&args;
+  void* kargs[] = {const_cast<void*>(karg)};
   hipError_t e = hipLaunchKernel((const void*)L.fn, dim3((unsigned)grid), dim3((unsigned)L.threads),
                                  kargs, 0, st);
   if (e == hipSuccess) e = hipGetLastError();
@@ -322,8 +324,44 @@ dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V,
   const int es = esize_of(dtype);
   const bool aligned = aligned16(logits) && ((ld * es) % 16 == 0);
   const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
-  dppo::RowArgs a{};
+  dppo::RowArgsV a{};
   a.logits = logits;
+  a.ld = ld;
+  a.ids = token_ids;
+  a.lp_out = logp_out;
+  a.lse_out = lse_out;
+  a.T = (int32_t)T;
+  a.V = (int32_t)V;
+  a.mode = dppo::kModeLogprob;
+  return launch_rows(L, a, T, (hipStream_t)stream);
+}
+
+dppo_status logprob_fwd_versioned(const void* const* logits, int32_t K, int32_t dtype, int64_t T,
+                                  int64_t V, int64_t ld, const int32_t* version_ids,
+                                  const int64_t* token_ids, float* logp_out, float* lse_out,
+                                  void* stream) {
+  if (K < 1 || K > DPPO_MAX_VERSIONS)
+    return fail(DPPO_ERR_INVALID_ARG, "K = %d versions out of [1, %d]", (int)K, DPPO_MAX_VERSIONS);
+  if (T > 0 && !logits) return fail(DPPO_ERR_INVALID_ARG, "logits pointer array is NULL");
+  for (int v = 0; v < K && T > 0; ++v) {
+    dppo_status s = check_matrix(logits[v], dtype, T, V, ld, "logits[v]");
+    if (s != DPPO_OK) return s;
+  }
+  if (T == 0) {
+    dppo_status s = check_matrix(nullptr, dtype, T, V, ld, "logits");
+    return s;
+  }
+  if (!version_ids || !token_ids || !logp_out)
+    return fail(DPPO_ERR_INVALID_ARG, "version_ids, token_ids and logp_out are required");
+  const int es = esize_of(dtype);
+  bool aligned = (ld * es) % 16 == 0;
+  for (int v = 0; v < K; ++v) aligned = aligned && aligned16(logits[v]);
+  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
+  dppo::RowArgsV a{};
+  a.logits = logits[0];
+  a.version = version_ids;
+  a.nver = K;
+  for (int v = 0; v < K; ++v) a.vlogits[v] = logits[v];
   a.ld = ld;
   a.ids = token_ids;
   a.lp_out = logp_out;
@@ -362,7 +400,7 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
     const bool aligned = aligned16(logits) && ((ld * es) % 16 == 0) &&
                          (!dlogits || (aligned16(dlogits) && (ld_dlogits * es) % 16 == 0));
     const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, dlogits != nullptr, g_path_policy);
-    dppo::RowArgs a{};
+    dppo::RowArgsV a{};
     a.logits = logits;
     a.ld = ld;
     a.dlogits = dlogits;

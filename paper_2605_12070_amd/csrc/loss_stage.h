@@ -4,6 +4,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
+#include "dppo.h"
+
 namespace dppo {
 
 constexpr int kModeLogprob = 0;  // log-prob (and lse) only
@@ -14,7 +18,7 @@ constexpr int kForceStream = 1;  // use the two-pass streaming kernel even when 
 
 // Arguments of every per-row kernel (passed by value).
 struct RowArgs {
-  const void* logits;
+  const void* logits;   // row t at logits + t * ld (RowArgsV: unless a version table is set)
   int64_t ld;
   void* dlogits;        // NULL: forward only
   int64_t ldd;
@@ -41,10 +45,21 @@ struct RowArgs {
   float alpha;          // behaviour-policy weight of an interpolated reference
 };
 
-typedef void (*RowKernel)(RowArgs);
+// Arguments of the kernels without the backward sweep: the row arguments plus an optional
+// per-token version table (versioned log-prob call). The gradient kernels take RowArgs
+// alone, so their argument block is not widened by a table they never read.
+struct RowArgsV : RowArgs {
+  const int32_t* version;                  // per-token policy version, or NULL
+  int32_t nver;                            // number of versions (1..DPPO_MAX_VERSIONS)
+  const void* vlogits[DPPO_MAX_VERSIONS];  // version v's logits; row t at vlogits[v] + t * ld
+};
+
+template <bool BWD>
+using RowArgsOf = typename std::conditional<BWD, RowArgs, RowArgsV>::type;
 
 struct RowLaunch {
-  RowKernel fn = nullptr;
+  const void* fn = nullptr;  // kernel taking RowArgsOf<bwd>
+  bool bwd = false;
   int threads = 0;
   int chunks = 0;            // resident kernels: 16-byte chunks per thread
   bool resident = false;

@@ -15,6 +15,38 @@
 
 namespace dppo {
 
+// Logits matrix holding token row `row`: with a version table (RowArgsV), the matrix of the
+// token's policy version. An out-of-range version reads version 0's matrix (always mapped)
+// and version_ok rejects the token. The pointer is picked with a chain of uniform selects:
+// indexing the by-value argument array with a run-time index would make the compiler copy
+// the arguments to scratch.
+template <class A>
+__device__ __forceinline__ const void* logits_of(const A& a, int64_t row) {
+  const void* base = a.logits;
+  if constexpr (std::is_same<A, RowArgsV>::value) {
+    if (a.version) {
+      const int v = (int)uload((const uint32_t*)(a.version + row));
+#pragma unroll
+      for (int i = 1; i < DPPO_MAX_VERSIONS; ++i)
+        if (v == i && i < a.nver) base = a.vlogits[i];
+    }
+  }
+  return base;
+}
+template <class T, class A>
+__device__ __forceinline__ const T* row_ptr(const A& a, int64_t row) {
+  return (const T*)logits_of(a, row) + row * a.ld;
+}
+template <class A>
+__device__ __forceinline__ bool version_ok(const A& a, int64_t row) {
+  if constexpr (std::is_same<A, RowArgsV>::value) {
+    if (!a.version) return true;
+    const int v = (int)uload((const uint32_t*)(a.version + row));
+    return v >= 0 && v < a.nver;
+  }
+  return true;
+}
+
 // Rows that are not evaluated (loss mask 0, or a bad token id on a valid row).
 template <typename Tin, int NT>
 __device__ void skip_row(const RowArgs& a, int64_t row, bool valid) {
@@ -108,7 +140,7 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 //           next row's first wait also wait for that store.
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD>
-__global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
+__global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
   __shared__ float red[2][2 * (NT / 64)];   // alternated by row parity: one barrier per merge
   __shared__ Bcast bc;
   // Per-chunk shifts n_c live in LDS (NC x NT floats, conflict-free [c][tid] layout): the
@@ -141,7 +173,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
   bool rd_cur = row < a.T && reads(row);
   {
     const __amdgpu_buffer_rsrc_t rz =
-        row_rsrc((const uint16_t*)a.logits + (rd_cur ? row : 0) * a.ld, rd_cur ? a.V * 2 : 0);
+        row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
   }
@@ -164,7 +196,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
     const int64_t next = row + gridDim.x;
     const bool rd_next = next < a.T && reads(next);
     const int64_t y = uload(a.ids + row);
-    const bool good = (y >= 0) && (y < V);
+    const bool good = (y >= 0) && (y < V) && version_ok(a, row);
     const TokenIn tin = token_inputs(a, row);   // scalar loads, in flight during pass A
     float w = 0.0f, dy = 0.0f, l2 = 0.0f;
 
@@ -174,7 +206,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
       float zy = 0.0f;
       if (good) {
         const uint64_t off = (uint64_t)(row * a.ld + y) * 2u;
-        const uint32_t wv = uload((const uint32_t*)((const char*)a.logits + (off & ~(uint64_t)3)));
+        const uint32_t wv = uload((const uint32_t*)((const char*)logits_of(a, row) + (off & ~(uint64_t)3)));
         zy = (off & 2u) ? bf16_hi(wv) : bf16_lo(wv);
       }
       // Pass A.
@@ -247,7 +279,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
     uint16_t* drow = want_d ? (uint16_t*)a.dlogits + row * a.ldd : nullptr;
     const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, (want_d && rd_cur) ? V * 2 : 0);
     const __amdgpu_buffer_rsrc_t rn = row_rsrc(
-        (const uint16_t*)a.logits + (rd_next ? next : row) * a.ld, rd_next ? V * 2 : 0);
+        row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
     const float wf = rd_cur ? w : 0.0f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -296,7 +328,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgs a) {
 // Register-resident row kernel, fp32 logits (4 per 16-byte chunk; exps stored as fp32).
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD>
-__global__ __launch_bounds__(NT) void rows_f32_resident(RowArgs a) {
+__global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
   const int64_t row = blockIdx.x;
@@ -306,12 +338,12 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgs a) {
   const bool loss_mode = a.mode != kModeLogprob;
   const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
   const int64_t y = a.ids[row];
-  const bool good = (y >= 0) && (y < V);
+  const bool good = (y >= 0) && (y < V) && version_ok(a, row);
   if (loss_mode && !(valid && good)) {
     skip_row_resident<NT, NC, 4>(a, row, valid);
     return;
   }
-  const float* zrow = (const float*)a.logits + row * a.ld;
+  const float* zrow = row_ptr<float>(a, row);
   float zy = 0.0f;
   if (tid == 0 && good) zy = zrow[y];
 
@@ -479,7 +511,7 @@ struct Chunk {
 };
 
 template <typename Tin, int NT, bool BWD, bool VEC>
-__global__ __launch_bounds__(NT) void rows_stream(RowArgs a) {
+__global__ __launch_bounds__(NT) void rows_stream(RowArgsOf<BWD> a) {
   using C = Chunk<Tin, VEC>;
   constexpr int E = C::E;
   __shared__ float red[2 * (NT / 64) + 2];
@@ -491,12 +523,12 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgs a) {
   const bool loss_mode = a.mode != kModeLogprob;
   const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
   const int64_t y = a.ids[row];
-  const bool good = (y >= 0) && (y < V);
+  const bool good = (y >= 0) && (y < V) && version_ok(a, row);
   if (loss_mode && !(valid && good)) {
     skip_row<Tin, NT>(a, row, valid);
     return;
   }
-  const Tin* zrow = (const Tin*)a.logits + row * a.ld;
+  const Tin* zrow = row_ptr<Tin>(a, row);
   float zy = 0.0f;
   if (tid == 0 && good) zy = load_elem<Tin>(zrow, y);
 
@@ -604,39 +636,40 @@ constexpr ResCfg kResident[] = {{256, 1},  {256, 2},   {256, 4},   {512, 4},   {
 constexpr int kNumResident = sizeof(kResident) / sizeof(kResident[0]);
 
 template <bool BWD>
-RowKernel pick_bf16(int i) {
+const void* pick_bf16(int i) {
   switch (i) {
-    case 0: return rows_bf16_resident<256, 1, BWD>;
-    case 1: return rows_bf16_resident<256, 2, BWD>;
-    case 2: return rows_bf16_resident<256, 4, BWD>;
-    case 3: return rows_bf16_resident<512, 4, BWD>;
-    case 4: return rows_bf16_resident<512, 6, BWD>;
-    case 5: return rows_bf16_resident<512, 8, BWD>;
-    case 6: return rows_bf16_resident<1024, 6, BWD>;
-    case 7: return rows_bf16_resident<1024, 8, BWD>;
-    case 8: return rows_bf16_resident<1024, 12, BWD>;
-    default: return rows_bf16_resident<1024, 19, BWD>;
+    case 0: return (const void*)rows_bf16_resident<256, 1, BWD>;
+    case 1: return (const void*)rows_bf16_resident<256, 2, BWD>;
+    case 2: return (const void*)rows_bf16_resident<256, 4, BWD>;
+    case 3: return (const void*)rows_bf16_resident<512, 4, BWD>;
+    case 4: return (const void*)rows_bf16_resident<512, 6, BWD>;
+    case 5: return (const void*)rows_bf16_resident<512, 8, BWD>;
+    case 6: return (const void*)rows_bf16_resident<1024, 6, BWD>;
+    case 7: return (const void*)rows_bf16_resident<1024, 8, BWD>;
+    case 8: return (const void*)rows_bf16_resident<1024, 12, BWD>;
+    default: return (const void*)rows_bf16_resident<1024, 19, BWD>;
   }
 }
 template <bool BWD>
-RowKernel pick_f32(int i) {
+const void* pick_f32(int i) {
   switch (i) {
-    case 0: return rows_f32_resident<256, 1, BWD>;
-    case 1: return rows_f32_resident<256, 2, BWD>;
-    case 2: return rows_f32_resident<256, 4, BWD>;
-    case 3: return rows_f32_resident<512, 4, BWD>;
-    case 4: return rows_f32_resident<512, 6, BWD>;
-    case 5: return rows_f32_resident<512, 8, BWD>;
-    case 6: return rows_f32_resident<1024, 6, BWD>;
-    case 7: return rows_f32_resident<1024, 8, BWD>;
-    case 8: return rows_f32_resident<1024, 12, BWD>;
-    default: return rows_f32_resident<1024, 19, BWD>;
+    case 0: return (const void*)rows_f32_resident<256, 1, BWD>;
+    case 1: return (const void*)rows_f32_resident<256, 2, BWD>;
+    case 2: return (const void*)rows_f32_resident<256, 4, BWD>;
+    case 3: return (const void*)rows_f32_resident<512, 4, BWD>;
+    case 4: return (const void*)rows_f32_resident<512, 6, BWD>;
+    case 5: return (const void*)rows_f32_resident<512, 8, BWD>;
+    case 6: return (const void*)rows_f32_resident<1024, 6, BWD>;
+    case 7: return (const void*)rows_f32_resident<1024, 8, BWD>;
+    case 8: return (const void*)rows_f32_resident<1024, 12, BWD>;
+    default: return (const void*)rows_f32_resident<1024, 19, BWD>;
   }
 }
 }  // namespace
 
 RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force) {
   RowLaunch L;
+  L.bwd = bwd;
   const int esize = dtype == DPPO_BF16 ? 2 : 4;
   const int64_t chunks = (V * esize + 15) / 16;
   int pick = -1;
@@ -661,11 +694,15 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   L.threads = 1024;
   L.resident = false;
   if (dtype == DPPO_BF16) {
-    L.fn = aligned ? (bwd ? rows_stream<uint16_t, 1024, true, true> : rows_stream<uint16_t, 1024, false, true>)
-                   : (bwd ? rows_stream<uint16_t, 1024, true, false> : rows_stream<uint16_t, 1024, false, false>);
+    L.fn = aligned ? (bwd ? (const void*)rows_stream<uint16_t, 1024, true, true>
+                          : (const void*)rows_stream<uint16_t, 1024, false, true>)
+                   : (bwd ? (const void*)rows_stream<uint16_t, 1024, true, false>
+                          : (const void*)rows_stream<uint16_t, 1024, false, false>);
   } else {
-    L.fn = aligned ? (bwd ? rows_stream<float, 1024, true, true> : rows_stream<float, 1024, false, true>)
-                   : (bwd ? rows_stream<float, 1024, true, false> : rows_stream<float, 1024, false, false>);
+    L.fn = aligned ? (bwd ? (const void*)rows_stream<float, 1024, true, true>
+                          : (const void*)rows_stream<float, 1024, false, true>)
+                   : (bwd ? (const void*)rows_stream<float, 1024, true, false>
+                          : (const void*)rows_stream<float, 1024, false, false>);
   }
   return L;
 }

@@ -309,3 +309,22 @@ def test_lm_head_workspace_size():
     assert L.fused_lm_head_workspace_bytes(T, d, V, 16384) < n
     assert L.fused_lm_head_workspace_bytes(T, 4, V, 0) == -1
     assert L.fused_lm_head_workspace_bytes(-1, d, V, 0) == -1
+
+
+@pytest.mark.parametrize("K,frag", [(0, "versions"), (9, "versions")])
+def test_versioned_logprob_rejects_bad_k(K, frag):
+    arr = (C.c_void_p * 9)(*([FAKE] * 9))
+    st = _lib.lib().logprob_fwd_versioned(arr, K, 1, 4, 8, 8, FAKE, FAKE, FAKE, None, None)
+    assert st == _lib.DPPO_ERR_INVALID_ARG
+    assert frag in _lib.lib().dppo_last_error().decode()
+
+
+def test_versioned_logprob_rejects_null_pointers():
+    L = _lib.lib()
+    arr = (C.c_void_p * 2)(FAKE, None)
+    assert L.logprob_fwd_versioned(arr, 2, 1, 4, 8, 8, FAKE, FAKE, FAKE, None, None) == _lib.DPPO_ERR_INVALID_ARG
+    arr = (C.c_void_p * 2)(FAKE, FAKE)
+    assert L.logprob_fwd_versioned(arr, 2, 1, 4, 8, 8, None, FAKE, FAKE, None, None) == _lib.DPPO_ERR_INVALID_ARG
+    assert L.logprob_fwd_versioned(None, 2, 1, 4, 8, 8, FAKE, FAKE, FAKE, None, None) == _lib.DPPO_ERR_INVALID_ARG
+    # T = 0 is a no-op that touches nothing
+    assert L.logprob_fwd_versioned(None, 1, 1, 0, 8, 8, None, None, None, None, None) == _lib.DPPO_OK

@@ -117,3 +117,27 @@ def test_out_of_range_ids_give_nan():
     z = np.zeros((3, 4))
     lp, _ = oracle.logprob_fwd(z, np.array([-1, 4, 3]))
     assert np.isnan(lp[0]) and np.isnan(lp[1]) and abs(lp[2] + math.log(4)) < 1e-15
+
+
+def test_versioned_logprob_special_cases():
+    """One version for every token reduces to the plain log-prob of that version's logits;
+    identical versions reduce to the plain log-prob; unknown versions give NaN."""
+    rng = np.random.default_rng(11)
+    T, V = 40, 37
+    zs = [rng.normal(0, 2, (T, V)) for _ in range(3)]
+    ids = rng.integers(0, V, T)
+    for v in range(3):
+        lp, _ = oracle.logprob_fwd(zs[v], ids)
+        np.testing.assert_array_equal(oracle.versioned_logprob(zs, np.full(T, v), ids), lp)
+    lp0, _ = oracle.logprob_fwd(zs[0], ids)
+    mixed = rng.integers(0, 3, T)
+    np.testing.assert_array_equal(oracle.versioned_logprob([zs[0]] * 3, mixed, ids), lp0)
+    bad = mixed.copy()
+    bad[:5] = [-1, 3, 7, -2, 100]
+    got = oracle.versioned_logprob(zs, bad, ids)
+    assert np.isnan(got[:5]).all() and np.isfinite(got[5:]).all()
+    # each token takes its own version's row, brute force on a tiny case
+    for t in range(T):
+        z = zs[mixed[t]][t]
+        ref = z[ids[t]] - np.log(np.sum(np.exp(z)))
+        assert abs(oracle.versioned_logprob(zs, mixed, ids)[t] - ref) < 1e-12

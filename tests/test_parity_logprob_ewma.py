@@ -146,3 +146,35 @@ def test_ewma_controller_resets_on_low_rho():
     cf = oracle.ewma_closed_form([np.full(n, 3.0), np.full(n, 4.0)], 0.75)
     np.testing.assert_allclose(ctl.x.cpu().numpy(), cf, rtol=1e-6)
     assert ctl.resets == 1 and abs(ctl.w - 1.75) < 1e-12
+
+
+@pytest.mark.parametrize("dtype,V,K,policy", [
+    (torch.bfloat16, 1000, 3, "auto"),          # ragged V: streaming kernel
+    (torch.bfloat16, 151936, 2, "auto"),        # register-resident persistent kernel
+    (torch.bfloat16, 32000, 4, "stream"),
+    (torch.float32, 4096, 4, "auto"),           # fp32 resident kernel
+])
+def test_logprob_versioned(dtype, V, K, policy):
+    """Each token reads the logits of its own policy version; unknown versions give NaN."""
+    T = 150
+    _say("logprob versioned", dtype, V, K, policy)
+    g = torch.Generator(device=DEV).manual_seed(V + K)
+    zs = [(3.0 * torch.randn(T, V, generator=g, device=DEV)).to(dtype) for _ in range(K)]
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ver = torch.randint(0, K, (T,), generator=g, device=DEV, dtype=torch.int32)
+    ver[:4] = torch.tensor([-1, K, 99, -7], dtype=torch.int32, device=DEV)
+    ids[5] = V + 1                               # bad id on a good version
+    P.set_path_policy(policy)
+    try:
+        lp, lse = P.logprob_fwd_versioned(zs, ver, ids, with_lse=True)
+        torch.cuda.synchronize()
+    finally:
+        P.set_path_policy("auto")
+    ref = oracle.versioned_logprob([bits_of(z) for z in zs], ver.cpu().numpy(), ids.cpu().numpy())
+    got = lp.cpu().double().numpy()
+    bad = np.array([0, 1, 2, 3, 5])
+    assert np.isnan(got[bad]).all() and np.isnan(ref[bad]).all()
+    assert np.isfinite(got[4]) and np.isfinite(ref[4])
+    ok = ~np.isnan(ref)
+    err = np.abs(got[ok] - ref[ok]) / np.maximum(np.abs(ref[ok]), 1.0)
+    assert err.max() < 2e-5, err.max()
