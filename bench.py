@@ -145,6 +145,45 @@ def ewma_bandwidth(dev, n, reps=20):
             "n": n, "dtype": "f32", "alg_bytes_per_launch": 12 * n, "kernel_ms": round(ms, 4)}
 
 
+def versioned_logprob_measure(dev, wl, K=4, reps=20):
+    """Exact old log-probs of a partial-rollout batch: K per-version logits matrices of the
+    batch's shape (version 0 is the batch's own logits, the others fresh N(0, 3^2) draws) and
+    a per-token version id (1..4 segments per sequence); each token's row is read from its
+    version only. Algorithmic bytes: T V esize + 16 B per token (id, version, log-prob)."""
+    T, V = wl.T, wl.V
+    g = torch.Generator(device=dev).manual_seed(11)
+    mats = [wl.logits]
+    for _ in range(K - 1):
+        z = torch.empty(T, V, dtype=wl.logits.dtype, device=dev)
+        for a in range(0, T, 2048):
+            z[a:a + 2048] = (3.0 * torch.randn(min(2048, T - a), V, generator=g, device=dev)).to(z.dtype)
+        mats.append(z)
+    ver = torch.as_tensor(W.version_ids(T, wl.seq_len, seed=12) % K, device=dev)
+    lp = P.logprob_fwd_versioned(mats, ver, wl.ids)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with P.KernelTimer() as kt:
+        e0.record(stream)
+        for _ in range(reps):
+            lp = P.logprob_fwd_versioned(mats, ver, wl.ids)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        k_ms, k_n = kt.read()
+    call_ms = e0.elapsed_time(e1) / reps
+    ms = k_ms / max(1, k_n)
+    b_alg = T * V * wl.logits.element_size() + 16 * T
+    gbps = b_alg / (ms * 1e-3) / 1e9
+    counts = np.bincount(ver.cpu().numpy(), minlength=K).tolist()
+    del mats, lp
+    return {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(gbps / HBM_PEAK_GBPS, 4),
+            "kernel": P.row_kernel_name(wl.logits.dtype, V, with_dlogits=False),
+            "kernel_ms": round(ms, 4), "alg_bytes_per_launch": b_alg, "versions": K,
+            "tokens_per_version": counts, "call_ms": round(call_ms, 4),
+            "tokens_per_s": round(T / (call_ms * 1e-3), 1)}
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, AMD specification
 
 
@@ -204,6 +243,8 @@ def main():
                     help="size of the parameter-sized EWMA measurement (0 to skip)")
     ap.add_argument("--no-lm-head", action="store_true",
                     help="skip the fused LM-head measurement")
+    ap.add_argument("--no-versioned", action="store_true",
+                    help="skip the versioned log-prob measurement")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -292,6 +333,10 @@ def main():
         "hbm_pct_of_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "roofline": roofline,
     }
+    if not args.no_versioned:
+        log("versioned log-prob")
+        del dlogits
+        result["versioned_logprob_roofline"] = versioned_logprob_measure(dev, wl)
     if args.ewma_elems > 0:
         result["ewma_roofline"] = ewma_bandwidth(dev, args.ewma_elems)
     if not args.no_lm_head:

@@ -325,6 +325,102 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
 }
 
 // ---------------------------------------------------------------------------------------
+// Forward-only row kernel, bf16 logits (log-prob calls, versioned or not, and the loss
+// without dlogits): persistent like rows_bf16_resident, NT threads x NC 16-byte chunks per
+// row. With no backward sweep a chunk's registers are free as soon as the chunk has been
+// unpacked, so the next row's chunk is loaded into them at once: the next row streams in
+// while this row is summed, merged and finished, and the loop waits for memory only at its
+// top. Rows that are not read (masked or bad-id loss rows) still run the chunk loop on
+// zeros, so that every row issues its successor's loads from the same place.
+// ---------------------------------------------------------------------------------------
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
+  __shared__ float red[2][2 * (NT / 64)];
+  __shared__ Bcast bc;
+  const bool loss_mode = a.mode != kModeLogprob;
+  auto reads = [&](int64_t rr) -> bool {
+    if (!loss_mode) return true;
+    if (a.mask != nullptr && uload_u8(a.mask + rr) == 0) return false;
+    const int64_t yy = uload(a.ids + rr);
+    return yy >= 0 && yy < a.V;
+  };
+  uint32_t r[NC][4];
+  int64_t row = blockIdx.x;
+  if (a.T >= 4 * (int64_t)gridDim.x) {      // staggered starts, as in rows_bf16_resident
+    const int steps = (int)((blockIdx.x >> 3) & 31);
+    for (int i = 0; i < steps; ++i) __builtin_amdgcn_s_sleep(12);
+  }
+  bool rd_cur = row < a.T && reads(row);
+  {
+    const __amdgpu_buffer_rsrc_t rz =
+        row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
+  }
+  int parity = 0;
+  for (; row < a.T; row += gridDim.x, parity ^= 1) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    const int tid = threadIdx.x;
+    const int V = a.V;
+    const int voff = tid * 16;
+    const int nfull = V >> 3;
+    const int cb = nfull / NT;
+    const bool lane_in = tid < nfull - cb * NT;
+    const int64_t next = row + gridDim.x;
+    const bool rd_next = next < a.T && reads(next);
+    const __amdgpu_buffer_rsrc_t rn =
+        row_rsrc(row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
+    const int64_t y = uload(a.ids + row);
+    const bool good = (y >= 0) && (y < V) && version_ok(a, row);
+    const TokenIn tin = token_inputs(a, row);
+    float zy = 0.0f;
+    if (rd_cur && good) {
+      const uint64_t off = (uint64_t)(row * a.ld + y) * 2u;
+      const uint32_t wv = uload((const uint32_t*)((const char*)logits_of(a, row) + (off & ~(uint64_t)3)));
+      zy = (off & 2u) ? bf16_hi(wv) : bf16_lo(wv);
+    }
+    float N = -INFINITY, S = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      float x[8];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x[2 * k] = bf16_lo(r[c][k]);
+        x[2 * k + 1] = bf16_hi(r[c][k]);
+      }
+      load16(r[c], rn, voff, c * NT * 16);
+      const float cm = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
+      float nc = __builtin_ceilf(cm * kLog2e);
+      const float sh = (nc == -INFINITY) ? 0.0f : nc;
+      // the same operations in the same order as rows_bf16_resident's pass A, so that the
+      // forward-only and the gradient calls return bit-identical log-probs and losses
+      float e[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) e[j] = exp2_hw(__builtin_fmaf(x[j], kLog2e, -sh));
+      const float sc = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+      const bool dead = (c > cb) || (c == cb && !lane_in);
+      merge_ns_int(N, S, dead ? -INFINITY : nc, dead ? 0.0f : sc);
+      // Pin the chunk's work here: otherwise the exponentials are sunk past the later
+      // chunks and every chunk's unpacked values stay live at once.
+      asm volatile("" : "+v"(N), "+v"(S));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (rd_cur) {
+      block_merge_ns_int<NT>(N, S, red[parity]);
+      const float lse2 = (N == -INFINITY) ? __builtin_nanf("") : N + log2f(S);
+      finish_row(a, row, zy, lse2, good, &bc, tin);
+    } else if (tid == 0) {                  // masked row, or a bad id on a valid loss row
+      const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
+      a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
+      a.loss_tok[row] = 0.0f;
+      if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
+      if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+    }
+    rd_cur = rd_next;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
 // Register-resident row kernel, fp32 logits (4 per 16-byte chunk; exps stored as fp32).
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD>
@@ -635,6 +731,20 @@ constexpr ResCfg kResident[] = {{256, 1},  {256, 2},   {256, 4},   {512, 4},   {
                                 {512, 8},  {1024, 6}, {1024, 8}, {1024, 12}, {1024, 19}};
 constexpr int kNumResident = sizeof(kResident) / sizeof(kResident[0]);
 
+const void* pick_bf16_fwd(int i) {
+  switch (i) {
+    case 0: return (const void*)rows_bf16_fwd<256, 1>;
+    case 1: return (const void*)rows_bf16_fwd<256, 2>;
+    case 2: return (const void*)rows_bf16_fwd<256, 4>;
+    case 3: return (const void*)rows_bf16_fwd<512, 4>;
+    case 4: return (const void*)rows_bf16_fwd<512, 6>;
+    case 5: return (const void*)rows_bf16_fwd<512, 8>;
+    case 6: return (const void*)rows_bf16_fwd<1024, 6>;
+    case 7: return (const void*)rows_bf16_fwd<1024, 8>;
+    case 8: return (const void*)rows_bf16_fwd<1024, 12>;
+    default: return (const void*)rows_bf16_fwd<1024, 19>;
+  }
+}
 template <bool BWD>
 const void* pick_bf16(int i) {
   switch (i) {
@@ -685,7 +795,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   if (pick >= 0) {
     L.threads = kResident[pick].nt;
     L.chunks = kResident[pick].nc;
-    L.fn = dtype == DPPO_BF16 ? (bwd ? pick_bf16<true>(pick) : pick_bf16<false>(pick))
+    L.fn = dtype == DPPO_BF16 ? (bwd ? pick_bf16<true>(pick) : pick_bf16_fwd(pick))
                               : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
     L.resident = true;
     L.persistent = dtype == DPPO_BF16;

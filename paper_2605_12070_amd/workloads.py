@@ -169,6 +169,15 @@ def _segments(rng, seq_len, max_segments=4):
     return gap
 
 
+def version_ids(T: int, seq_len: int, seed: int) -> np.ndarray:
+    """Per-token policy version of a partial-rollout batch: sequences of seq_len tokens, each
+    cut into 1..4 segments as in _segments, version id = staleness gap (0 = newest)."""
+    rng = np.random.default_rng(seed)
+    n_seq = -(-T // seq_len) if T > 0 else 0
+    gaps = [_segments(rng, min(seq_len, T - i * seq_len)) for i in range(n_seq)]
+    return (np.concatenate(gaps) if gaps else np.zeros(0, np.int64)).astype(np.int32)
+
+
 def make_workload(name: str, device="cpu", T: int | None = None, V: int | None = None,
                   seed: int | None = None, seq_len: int | None = None) -> Workload:
     """Draw one named workload. T, V, seed and seq_len may be overridden (parity sizes)."""

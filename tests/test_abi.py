@@ -195,7 +195,8 @@ def test_row_kernel_name_follows_the_selection_rule():
     assert row_kernel_name(bf, 151936) == "dppo::rows_bf16_resident<1024, 19, true>"
     assert row_kernel_name(bf, 155648) == "dppo::rows_bf16_resident<1024, 19, true>"
     assert row_kernel_name(bf, 155656).startswith("dppo::rows_stream<unsigned short, 1024, true")
-    assert row_kernel_name(bf, 151936, with_dlogits=False).endswith("<1024, 19, false>")
+    assert row_kernel_name(bf, 151936, with_dlogits=False) == "dppo::rows_bf16_fwd<1024, 19>"
+    assert row_kernel_name(f32, 32000, with_dlogits=False) == "dppo::rows_f32_resident<1024, 8, false>"
     assert row_kernel_name(bf, 2048) == "dppo::rows_bf16_resident<256, 1, true>"
     assert row_kernel_name(bf, 77825).startswith("dppo::rows_stream")      # ragged chunk
     assert row_kernel_name(bf, 64, ld=68).endswith("true, false>")          # unaligned stride

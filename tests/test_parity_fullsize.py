@@ -86,3 +86,39 @@ def test_long_agentic_fullsize():
     ref_prox = oracle.ewma_fixed_step(lp_prev.cpu().double().numpy(),
                                       lp_old.cpu().double().numpy(), 0.9)
     _check_workload(wl, prox, lp_mu, ref_prox)
+
+
+def test_versioned_logprob_fullsize():
+    """Exact old log-probs of a partial-rollout batch at the large-vocabulary size (T=16384,
+    V=151936, bf16, 4 policy versions, 1..4 version segments per 512-token sequence), as the
+    benchmark runs it: sampled rows of every version against the oracle, and on every row
+    bit-equality with logprob_fwd over that token's own version matrix."""
+    wl = W.make_workload("large_vocab", device=DEV)
+    T, V, K = wl.T, wl.V, 4
+    print(f"[case] fullsize versioned T={T} V={V} K={K}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(11)
+    zs = [wl.logits]
+    for _ in range(K - 1):
+        z = torch.empty(T, V, dtype=torch.bfloat16, device=DEV)
+        for a in range(0, T, 2048):
+            z[a:a + 2048] = (3.0 * torch.randn(min(2048, T - a), V, generator=g, device=DEV)).to(z.dtype)
+        zs.append(z)
+    ver_np = W.version_ids(T, wl.seq_len, seed=12) % K
+    ver = torch.as_tensor(ver_np, device=DEV)
+    lp = P.logprob_fwd_versioned(zs, ver, wl.ids)
+    torch.cuda.synchronize()
+    got = lp.cpu().numpy()
+    assert np.all(np.isfinite(got)) and np.all(got <= 0)
+    for v in range(K):
+        sel = ver_np == v
+        assert sel.any()
+        own = P.logprob_fwd(zs[v], wl.ids).cpu().numpy()
+        np.testing.assert_array_equal(got[sel], own[sel])
+    rng = np.random.default_rng(1)
+    rows = np.sort(np.concatenate([rng.choice(np.nonzero(ver_np == v)[0], 12, replace=False)
+                                   for v in range(K)]))
+    idx = torch.as_tensor(rows, device=DEV)
+    ref = oracle.versioned_logprob([bits_of(z[idx]) for z in zs], ver_np[rows],
+                                   wl.ids[idx].cpu().numpy())
+    err = np.abs(got[rows] - ref) / np.maximum(np.abs(ref), 1.0)
+    assert err.max() < 2e-5, err.max()

@@ -345,3 +345,27 @@ def test_interpolated_reference(kind, wl_name, T, n_gap, band, eps):
     edge = np.min(np.abs(np.log(r)[:, None] - bounds[None]), axis=1) < 1e-4
     assert np.array_equal(keep[~edge], keep_eff[~edge])
     _say("interpolated ref ok", kind, wl_name, "ties", n_ties, "kept", int(keep.sum()), "of", len(keep))
+
+
+@pytest.mark.parametrize("V", [1000, 8192, 32000, 77824, 151936, 155648])
+def test_forward_only_kernel_matches_gradient_call(V):
+    """The forward-only call (its own row kernel for bf16) returns bit-for-bit the values of
+    the call that also writes dlogits, on a batch with masked rows (40 %) and bad ids, and
+    both match the oracle."""
+    T = 96
+    _say("forward-only", V, T)
+    wl = W.make_workload("long_agentic", device=DEV, T=T, V=V, seq_len=48)
+    wl.ids[5] = V + 2
+    wl.ids[6] = -3
+    anchor = oracle_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor.to(DEV), wl)
+    fwd = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask,
+                                       want_dlogits=False)
+    both = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask)
+    torch.cuda.synchronize()
+    for f in ("logp", "loss_tok", "flags", "stats", "loss"):
+        a, b = getattr(fwd, f).cpu(), getattr(both, f).cpu()
+        assert torch.equal(a.nan_to_num(7.0), b.nan_to_num(7.0)), f
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    ref = run_oracle(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask, None, params)
+    compare_loss(both, ref, params, wl.logits.dtype)
