@@ -53,6 +53,18 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def recorded_traffic(key):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary, or None when
+    the kernel source has changed since the counters were taken."""
+    try:
+        tr = json.load(open(TRAFFIC_FILE)).get(key)
+    except (OSError, ValueError):
+        return None
+    if tr and tr.get("source_hash") == kernel_source_hash():
+        return tr["bytes_per_launch"]
+    return None
+
+
 def anchor_logprob(logits, ids, chunk=1024):
     """Sampled-token log-probs from PyTorch (float32), only to synthesise lp_ref / lp_mu."""
     T = logits.shape[0]
@@ -310,13 +322,7 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
                 "kernel": P.row_kernel_name(wl.logits.dtype, V),
                 "kernel_ms": round(k_ms, 4), "alg_bytes_per_launch": b_alg}
-    if os.path.exists(TRAFFIC_FILE):
-        try:
-            tr = json.load(open(TRAFFIC_FILE)).get(args.workload)
-            if tr and tr.get("source_hash") == kernel_source_hash():
-                roofline["traffic"] = tr["bytes_per_launch"]
-        except (OSError, ValueError):
-            pass
+    roofline["traffic"] = recorded_traffic(args.workload)
 
     result = {
         "metric": METRIC, "value": round(tokens_per_s, 1), "unit": "tokens/s",
@@ -336,7 +342,10 @@ def main():
     if not args.no_versioned:
         log("versioned log-prob")
         del dlogits
-        result["versioned_logprob_roofline"] = versioned_logprob_measure(dev, wl)
+        vr = versioned_logprob_measure(dev, wl)
+        if args.workload == "large_vocab":
+            vr["traffic"] = recorded_traffic("versioned_logprob")
+        result["versioned_logprob_roofline"] = vr
     if args.ewma_elems > 0:
         result["ewma_roofline"] = ewma_bandwidth(dev, args.ewma_elems)
     if not args.no_lm_head:
