@@ -24,26 +24,34 @@ namespace {
 // zeros for a lane whose offset lies outside the resource, which bounds every access to
 // the tile's rows and turns a K tail past d into zeros). There is no register staging:
 // LMH_STAGES LDS stages form a ring, and the loads of stage k + LMH_STAGES - 1 are issued
-// while stage k is multiplied. A stage holds the A and B tiles as 128-byte rows (64 bf16 of
-// K); the 16-byte chunk c of row r sits at position c ^ ((r / 2) % 8), so the fragment
+// while stage k is multiplied. A stage holds the A and B tiles as rows of LMH_BK bf16 of K
+// (64 or 128 bytes); the 16-byte chunk c of row r sits at position c ^ sw(r), with
+// sw(r) = (r / 2) % 8 for 128-byte rows and (r / 4) % 4 for 64-byte rows, so the fragment
 // reads of 16 lanes (16 consecutive rows, one chunk) cover all 64 banks. Each stage is its
 // own LDS object, which lets the compiler track the loads into each separately.
 // Wave (wm, wn) owns TM x TN tiles of 32 x 32 (v_mfma_f32_32x32x16_bf16, fp32 accumulation;
-// operand lane l holds row l % 32, K 8 (l / 32) .. +7). After the K loop, epi(Cs, mi, ldc)
-// runs in TM passes; pass mi stages, for every wave row wm, the 32 token rows
-// wm * 32 TM + mi * 32 + [0, 32) as Cs[s][col], s = wm * 32 + row % 32, col in [0, BN).
+// operand lane l holds row l % 32, K 8 (l / 32) .. +7). The vocabulary tile is the A operand,
+// so an accumulator holds vocabulary rows in its registers and tokens across its lanes: a
+// lane reduces over the vocabulary of its own tokens without crossing lanes (LmhLane below).
+// After the K loop, epi(acc, scratch) runs on the accumulators, with the ring as scratch.
 constexpr int kWaves = LMH_WM * LMH_WN;
-constexpr int kIA = LMH_BM / 8 / kWaves;        // loads per wave and stage, A (8 rows each)
-constexpr int kIB = LMH_BN / 8 / kWaves;        // and B
+constexpr int kChunks = LMH_BK / 8;             // 16-byte chunks per staged row
+constexpr int kRL = 64 / kChunks;               // rows covered by one wave-wide load
+constexpr int kIA = LMH_BM / kRL / kWaves;      // loads per wave and stage, A
+constexpr int kIB = LMH_BN / kRL / kWaves;      // and B
 constexpr int kAEl = LMH_BM * LMH_BK;           // bf16 elements of the A tile (B follows)
 constexpr int kStageEl = (LMH_BM + LMH_BN) * LMH_BK;
-constexpr int kRows = 32 * LMH_WM;              // staged rows per epilogue pass
-constexpr int kLdc = LMH_BN + 8;                // staged row stride (floats): rows 8 apart
-                                                // in bank, so 8 rows x 8 lanes are distinct
-static_assert(LMH_BK == 64 && LMH_BM % (8 * kWaves) == 0 && LMH_BN % (8 * kWaves) == 0,
+static_assert((LMH_BK == 64 || LMH_BK == 32) && LMH_BM % (kRL * kWaves) == 0 &&
+                  LMH_BN % (kRL * kWaves) == 0,
               "tile shape");
-static_assert(kRows * kLdc * 4 <= LMH_STAGES * kStageEl * 2, "an epilogue pass fits in the ring");
-static_assert(LMH_STAGES >= 2 && LMH_STAGES <= 4, "ring depth");
+static_assert(LMH_WM * LMH_TM * LMH_WN * 32 * 8 <= LMH_STAGES * kStageEl * 2,
+              "the forward merge scratch fits in the ring");
+static_assert(LMH_STAGES >= 2 && (LMH_STAGES - 2) * (kIA + kIB) <= 63, "ring depth");
+
+// Swizzled position of 16-byte chunk c in staged row r.
+__device__ __forceinline__ int lmh_sw(int r) {
+  return LMH_BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+}
 
 template <typename Epi>
 __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
@@ -59,33 +67,33 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
   const __amdgpu_buffer_rsrc_t ra = row_rsrc(m.hidden + (int64_t)m0 * d, rows_a * d * 2);
   const __amdgpu_buffer_rsrc_t rb = row_rsrc(m.weight + (int64_t)r0 * d, rows_b * d * 2);
 
-  // Load i of wave w covers tile rows 8 (w I + i) .. +7: lane l takes row 8 (w I + i) + l / 8
-  // at position l % 8, i.e. K chunk (l % 8) ^ ((row / 2) % 8).
+  // Load i of wave w covers tile rows kRL (w I + i) .. +kRL-1: lane l takes row
+  // kRL (w I + i) + l / kChunks at position l % kChunks, i.e. K chunk (l % kChunks) ^ sw(row).
   int goa[kIA], gob[kIB];
 #pragma unroll
   for (int i = 0; i < kIA; ++i) {
-    const int row = 8 * (wave * kIA + i) + (lane >> 3);
-    goa[i] = (row * d + ((lane & 7) ^ ((row >> 1) & 7)) * 8) * 2;
+    const int row = kRL * (wave * kIA + i) + lane / kChunks;
+    goa[i] = (row * d + ((lane % kChunks) ^ lmh_sw(row)) * 8) * 2;
   }
 #pragma unroll
   for (int i = 0; i < kIB; ++i) {
-    const int row = 8 * (wave * kIB + i) + (lane >> 3);
-    gob[i] = (row * d + ((lane & 7) ^ ((row >> 1) & 7)) * 8) * 2;
+    const int row = kRL * (wave * kIB + i) + lane / kChunks;
+    gob[i] = (row * d + ((lane % kChunks) ^ lmh_sw(row)) * 8) * 2;
   }
   auto issue = [&](uint16_t* s, int kb) {
     const int k0 = kb * BK;
 #pragma unroll
     for (int i = 0; i < kIA; ++i) {
-      const int row = 8 * (wave * kIA + i) + (lane >> 3);
-      const int kc = (lane & 7) ^ ((row >> 1) & 7);
+      const int row = kRL * (wave * kIA + i) + lane / kChunks;
+      const int kc = (lane % kChunks) ^ lmh_sw(row);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           ra, (__attribute__((address_space(3))) void*)(s + (wave * kIA + i) * 512), 16,
           (k0 + kc * 8 < d) ? goa[i] + k0 * 2 : 0x7fffff00, 0, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < kIB; ++i) {
-      const int row = 8 * (wave * kIB + i) + (lane >> 3);
-      const int kc = (lane & 7) ^ ((row >> 1) & 7);
+      const int row = kRL * (wave * kIB + i) + lane / kChunks;
+      const int kc = (lane % kChunks) ^ lmh_sw(row);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rb, (__attribute__((address_space(3))) void*)(s + kAEl + (wave * kIB + i) * 512), 16,
           (k0 + kc * 8 < d) ? gob[i] + k0 * 2 : 0x7fffff00, 0, 0, 0);
@@ -106,12 +114,12 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
 #pragma unroll
     for (int mi = 0; mi < TM; ++mi) {
       const int R = wm * 32 * TM + mi * 32 + (lane & 31);
-      af[mi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + R * BK + ((kc ^ ((R >> 1) & 7)) * 8)));
+      af[mi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + R * BK + ((kc ^ lmh_sw(R)) * 8)));
     }
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni) {
       const int R = wn * 32 * TN + ni * 32 + (lane & 31);
-      bfr[ni] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + kAEl + R * BK + ((kc ^ ((R >> 1) & 7)) * 8)));
+      bfr[ni] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + kAEl + R * BK + ((kc ^ lmh_sw(R)) * 8)));
     }
   };
   auto compute = [&](const uint16_t* s) {
@@ -125,7 +133,7 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
       for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mi], b0[ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0[ni], a0[mi], acc[mi][ni], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
       if (ks + 2 < BK / 16) frags(s, ks + 2, a0, b0);
       __builtin_amdgcn_sched_barrier(0);
@@ -133,7 +141,7 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
       for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mi], b1[ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1[ni], a1[mi], acc[mi][ni], 0, 0, 0);
     }
   };
   // Barrier without a memory fence (a fence would wait for the loads still in flight); the
@@ -157,9 +165,7 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
         // This wave's loads of stage kb are complete once at most the loads of the S - 2
         // later stages are outstanding; after the barrier, every wave's are.
         if (kb + S - 2 < nk) {
-          if constexpr (S == 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-          if constexpr (S == 3) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kIA + kIB) : "memory");
-          if constexpr (S == 4) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * (kIA + kIB)) : "memory");
+          asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 2) * (kIA + kIB)) : "memory");
         } else {
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         }
@@ -172,29 +178,26 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
   barrier();
 
-  // 32x32 accumulator layout: register r of lane l is row 8 (r / 4) + 4 (l / 32) + r % 4,
-  // column l % 32. The passes stage through the ring (its stages are contiguous).
-  float* Cs = (float*)st[0];
-#pragma unroll
-  for (int mi = 0; mi < TM; ++mi) {
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int s = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int col = wn * 32 * TN + ni * 32 + (lane & 31);
-        Cs[s * kLdc + col] = acc[mi][ni][r];
-      }
-    __syncthreads();
-    epi((const float*)Cs, mi, kLdc);
-    __syncthreads();
-  }
+  // The ring is free from here on; the epilogue works on the accumulators in registers and
+  // may use the ring as scratch.
+  epi(acc, (float*)st[0]);
 }
 
-// Token row of staged row s in pass mi.
-__device__ __forceinline__ int lmh_token(int m0, int s, int mi) {
-  return m0 + (s >> 5) * 32 * LMH_TM + mi * 32 + (s & 31);
-}
+// Accumulator layout (v_mfma_f32_32x32x16_bf16 with the vocabulary tile as the A operand):
+// acc[mi][ni] register r of lane l holds z for token
+//   m0 + wm 32 TM + mi 32 + l % 32
+// and vocabulary row
+//   r0 + wn 32 TN + ni 32 + 8 (r / 4) + 4 (l / 32) + r % 4,
+// so a lane sees one token per mi and, for each (ni, r / 4), four consecutive vocabulary rows.
+struct LmhLane {
+  int wm, wn, lane;
+  __device__ LmhLane() : wm((threadIdx.x >> 6) / LMH_WN), wn((threadIdx.x >> 6) % LMH_WN), lane(threadIdx.x & 63) {}
+  __device__ int token(int m0, int mi) const { return m0 + wm * 32 * LMH_TM + mi * 32 + (lane & 31); }
+  // tile-relative vocabulary row of register r of tile ni
+  __device__ int vrow(int ni, int r) const {
+    return wn * 32 * LMH_TN + ni * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+  }
+};
 
 }  // namespace
 
@@ -214,33 +217,53 @@ __global__ __launch_bounds__(LMH_THREADS) void lmh_fwd_tiles(LmhArgs m) {
   const int nt = blockIdx.y;
   const int r0 = m.n0 + nt * LMH_BN;
   const int ncols = min(LMH_BN, m.n1 - r0);
-  const int tid = threadIdx.x;
-  constexpr int TPR = LMH_THREADS / kRows;      // threads per staged row
-  constexpr int QC = LMH_BN / TPR;              // columns per thread
-  const int s = tid / TPR, q = tid % TPR;
-  auto epi = [&](const float* Cs, int mi, int ldc) {
-    // thread q of a row takes columns q, q + TPR, q + 2 TPR, ...: the TPR threads of a row
-    // read consecutive words, and the padded stride puts the rows of a wave in other banks
-    const float* cr = Cs + s * ldc + q;
-    float mx = -INFINITY;
-#pragma unroll 16
-    for (int j = 0; j < QC; ++j)
-      if (j * TPR + q < ncols) mx = fmaxf(mx, cr[j * TPR]);
-    const float m2 = mx * kLog2e;
-    float sum = 0.0f;
-    if (mx != -INFINITY) {
-#pragma unroll 16
-      for (int j = 0; j < QC; ++j)
-        if (j * TPR + q < ncols) sum += exp2_hw(__builtin_fmaf(cr[j * TPR], kLog2e, -m2));
-    }
-    float n = (mx == -INFINITY) ? -INFINITY : m2;
+  auto epi = [&](f32x16 (&acc)[LMH_TM][LMH_TN], float* scratch) {
+    const LmhLane L;
+    // scratch[wm][mi][wn][token] of (n, s): the LMH_WN waves that share a token row merge
+    // through LDS
+    float2* xs = (float2*)scratch;
+    const bool ragged = ncols < LMH_BN;       // only the last vocabulary tile
 #pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) merge_ns(n, sum, __shfl_xor(n, o, 64), __shfl_xor(sum, o, 64));
-    const int t = lmh_token(m0, s, mi);
-    if (q == 0 && t < m.T) {
-      float* p = m.part + ((int64_t)nt * m.T + t) * 2;
-      p[0] = n;
-      p[1] = sum;
+    for (int mi = 0; mi < LMH_TM; ++mi) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int ni = 0; ni < LMH_TN; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float x = acc[mi][ni][r];
+          mx = fmaxf(mx, (ragged && L.vrow(ni, r) >= ncols) ? -INFINITY : x);
+        }
+      const float m2 = mx * kLog2e;
+      const float sh = (mx == -INFINITY) ? 0.0f : m2;
+      float sum = 0.0f;
+#pragma unroll
+      for (int ni = 0; ni < LMH_TN; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = exp2_hw(__builtin_fmaf(acc[mi][ni][r], kLog2e, -sh));
+          sum += (ragged && L.vrow(ni, r) >= ncols) ? 0.0f : e;
+        }
+      float n = (mx == -INFINITY) ? -INFINITY : m2;
+      merge_ns(n, sum, __shfl_xor(n, 32, 64), __shfl_xor(sum, 32, 64));
+      if (L.lane < 32)
+        xs[((L.wm * LMH_TM + mi) * LMH_WN + L.wn) * 32 + L.lane] = make_float2(n, sum);
+    }
+    __syncthreads();
+    // one thread per token of the tile merges the LMH_WN partials
+    for (int i = threadIdx.x; i < LMH_BM; i += LMH_THREADS) {
+      const int wm = i / (32 * LMH_TM), mi = (i / 32) % LMH_TM, l = i % 32;
+      const int t = m0 + i;
+      float n = -INFINITY, sum = 0.0f;
+#pragma unroll
+      for (int wn = 0; wn < LMH_WN; ++wn) {
+        const float2 v = xs[((wm * LMH_TM + mi) * LMH_WN + wn) * 32 + l];
+        merge_ns(n, sum, v.x, v.y);
+      }
+      if (t < m.T) {
+        float* p = m.part + ((int64_t)nt * m.T + t) * 2;
+        p[0] = n;
+        p[1] = sum;
+      }
     }
   };
   LMH_RUN_ENGINE(m, m0, r0, epi);
@@ -330,36 +353,38 @@ __global__ __launch_bounds__(LMH_THREADS) void lmh_bwd_tiles(LmhArgs m) {
   const int m0 = blockIdx.x * LMH_BM;
   const int r0 = m.n0 + blockIdx.y * LMH_BN;
   const int ncols = min(LMH_BN, m.n1 - r0);
-  constexpr int GRP = LMH_BN / 4;                // 4-column groups of a staged row
-  auto epi = [&](const float* Cs, int mi, int ldc) {
-    // a wave covers 64 consecutive 4-column groups of one row: its 16-byte reads of 16
-    // lanes hit 64 distinct banks, and its 8-byte stores are contiguous
-#pragma unroll 2
-    for (int i = 0; i < kRows * GRP / LMH_THREADS; ++i) {
-      const int idx = threadIdx.x + LMH_THREADS * i;
-      const int s = idx / GRP, c0 = (idx % GRP) * 4;
-      const int t = lmh_token(m0, s, mi);
-      if (t >= m.T || c0 >= ncols) continue;
-      const bool ev = m.ev[t] != 0;
-      const float wt = m.w[t], l2 = m.lse2[t];
-      const int64_t y = m.ids[t];
-      const f32x4 x = *(const f32x4*)(Cs + s * ldc + c0);
-      float o[4];
+  auto epi = [&](f32x16 (&acc)[LMH_TM][LMH_TN], float*) {
+    const LmhLane L;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float p = exp2_hw(__builtin_fmaf(x[j], kLog2e, -l2));
-        const float oh = (int64_t)(r0 + c0 + j) == y ? 1.0f : 0.0f;
-        o[j] = ev ? wt * (p - oh) : 0.0f;
-      }
-      uint16_t* dst = m.g + (int64_t)t * m.ldg + (r0 - m.n0) + c0;
-      if (c0 + 4 <= ncols) {
-        u32x2 v;
-        v.x = pack_bf16(o[0], o[1]);
-        v.y = pack_bf16(o[2], o[3]);
-        *(u32x2*)dst = v;
-      } else {
-        for (int j = 0; j < ncols - c0; ++j) dst[j] = to_bf16(o[j]);
-      }
+    for (int mi = 0; mi < LMH_TM; ++mi) {
+      const int t = L.token(m0, mi);
+      if (t >= m.T) continue;
+      const bool ev = m.ev[t] != 0;
+      const float wt = ev ? m.w[t] : 0.0f;
+      const float l2 = m.lse2[t];
+      const int64_t yr = m.ids[t] - r0;        // the token's id relative to the tile
+      uint16_t* grow = m.g + (int64_t)t * m.ldg + (r0 - m.n0);
+#pragma unroll
+      for (int ni = 0; ni < LMH_TN; ++ni)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // four consecutive vocabulary rows v0 .. v0 + 3 of this token
+          const int v0 = L.vrow(ni, 4 * q);
+          float o[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float p = exp2_hw(__builtin_fmaf(acc[mi][ni][4 * q + j], kLog2e, -l2));
+            o[j] = ev ? wt * (p - ((int64_t)(v0 + j) == yr ? 1.0f : 0.0f)) : 0.0f;
+          }
+          if (v0 + 4 <= ncols) {
+            u32x2 v;
+            v.x = pack_bf16(o[0], o[1]);
+            v.y = pack_bf16(o[2], o[3]);
+            *(u32x2*)(grow + v0) = v;
+          } else {
+            for (int j = 0; j < 4 && v0 + j < ncols; ++j) grow[v0 + j] = to_bf16(o[j]);
+          }
+        }
     }
   };
   LMH_RUN_ENGINE(m, m0, r0, epi);
