@@ -88,7 +88,7 @@ def cpu_baseline(wl, lp_mu, lp_ref, rows, threads):
     params = oracle.Params(0.5, 2.0, 0.2, 0.2, "mask_weight", "token_mean", 1.0)
     scale = oracle.batch_scale(mask, params)
     idx = torch.as_tensor(rows, device=wl.logits.device)
-    z16 = wl.logits[idx].cpu()
+    z16 = (wl.logits if len(rows) == wl.T else wl.logits[idx]).cpu()
     if z16.dtype == torch.bfloat16:
         zb = z16.view(torch.int16).numpy().view(np.uint16)
         decode = oracle.bf16_bits_to_f64
@@ -248,7 +248,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="large_vocab", choices=sorted(W.WORKLOADS))
-    ap.add_argument("--cpu-rows", type=int, default=4096)
+    ap.add_argument("--cpu-rows", type=int, default=0,
+                    help="rows of the batch the oracle baseline runs on (0: the whole batch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy", action="store_true")
     ap.add_argument("--ewma-elems", type=int, default=1 << 30,
@@ -355,13 +356,16 @@ def main():
         result["context"] = {"d2d_copy_GBps": round(copy_bandwidth(dev), 1)}
     if not args.no_cpu_baseline:
         threads = min(16, len(os.sched_getaffinity(0)))
-        rows = np.sort(np.random.default_rng(0).choice(T, size=min(args.cpu_rows, T),
-                                                       replace=False))
+        if 0 < args.cpu_rows < T:
+            rows = np.sort(np.random.default_rng(0).choice(T, size=args.cpu_rows, replace=False))
+        else:
+            rows = np.arange(T)
         log(f"cpu baseline: oracle on {len(rows)} rows, {threads} threads")
         rate, dt = cpu_baseline(wl, lp_mu, lp_ref, rows, threads)
         result["cpu_baseline"] = {
             "value": round(rate, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{len(rows)} seeded rows of the {args.workload} batch (T={T}, V={V}), "
+            "sample": (f"the whole {args.workload} batch" if len(rows) == T else
+                       f"{len(rows)} seeded rows of the {args.workload} batch") + f" (T={T}, V={V}), "
                       f"float64 numpy oracle incl. dlogits, {dt:.1f} s wall",
             "cpu": platform.processor() or platform.machine()}
     print(json.dumps(result), flush=True)
