@@ -3,9 +3,9 @@
     python bench.py [--steps K] [--warmup W] [--workload large_vocab] [--no-cpu-baseline]
 
 A step is one pass of the whole loss stage over one batch: the fused kernel (valid-token
-count, per-row log-sum-exp / ratios / decisions / loss / dlogits, loss sum), the host
-reset controller reading the five stats (one device-to-host copy), and the PPO-EWMA
-update of the per-token proxy buffer. Inputs are synthetic, seeded, and resident in HBM
+count, per-row log-sum-exp / ratios / decisions / loss / dlogits, loss sum), then the reset
+controller reading the five stats and the PPO-EWMA update of the per-token proxy buffer,
+both on the device (no device-to-host copy inside the step). Inputs are synthetic, seeded, and resident in HBM
 before the timed region. Prints one JSON line.
 """
 from __future__ import annotations
@@ -286,14 +286,14 @@ def main():
     esize = wl.logits.element_size()
     dlogits = torch.empty_like(wl.logits)
     out = None
-    proxy = P.EwmaProxy(x_new, beta=P.beta_from_window(6), tau=0.9, patience=1)
+    proxy = P.EwmaProxyDevice(x_new, beta=P.beta_from_window(6), tau=0.9, patience=1)
     torch.cuda.synchronize()
 
     def step():
         nonlocal out
         out = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, mask,
                                            dlogits=dlogits, out=out)
-        proxy.step(x_new, out.stats)               # stats D2H + reset decision + EWMA
+        proxy.step(x_new, out.stats)               # reset rule + EWMA on the device, no sync
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):

@@ -244,6 +244,50 @@ dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, in
                               float beta, double* w, int32_t reset, int32_t normalized,
                               void* stream);
 
+/*
+ * Device-resident state of the PPO-EWMA reference and of its automatic reset (Sec. 5.2,
+ * App. B, App. E), for ewma_proxy_step. 40 bytes, 8-byte aligned, in device memory owned by
+ * the caller; checkpoint it together with the proxy buffer. Initialise with the host: w as
+ * for ewma_proxy_update (0 before the first step, 1 when the buffer already holds
+ * theta^(0)), every other field 0.
+ */
+typedef struct {
+  double w;           /* normaliser: w_{t-1} before a step, w_t after (normalized form)    */
+  int32_t streak;     /* consecutive steps with rho_t < tau, reset to 0 when a reset fires */
+  int32_t resets;     /* resets fired so far                                               */
+  int32_t last_reset; /* 1 when the last step reset the buffer, else 0                     */
+  int32_t error;      /* 1 when the last step found w negative or not finite; that step    */
+                      /* left the buffer and the state (other than this field) unchanged  */
+  float last_rho;     /* rho_t of the last step                                            */
+  float ca, cb;       /* coefficients of the last step: x_prox <- ca x_new + cb x_prox      */
+  int32_t reserved;
+} dppo_ewma_state;
+
+/*
+ * ewma_proxy_step -- the reset controller and the PPO-EWMA update of ewma_proxy_update,
+ * both on the device, so that a training step needs no device-to-host copy and no
+ * synchronisation (the reset rule of Sec. 5.2 and App. E; the recursion of Eq. 5 / App. B).
+ * A one-thread kernel reads the loss stage's counters and updates *state:
+ *    rho_t = n_active / n_valid (1 when n_valid = 0; stats NULL means rho_t = 1);
+ *    streak <- streak + 1 if rho_t < tau (compared in double), else 0;
+ *    a reset fires when streak >= patience; the streak then restarts at 0;
+ *    w_t and (ca, cb) exactly as ewma_proxy_update computes them on the host, in double,
+ *    then rounded to float.
+ * The element kernel then applies x_prox <- ca x_new + cb x_prox (x_prox not read when
+ * cb = 0) with the arithmetic of ewma_proxy_update, so both entry points give bit-identical
+ * buffers for the same sequence of reset decisions.
+ *  x_prox, x_new  [n] device buffers of `dtype`, as for ewma_proxy_update.
+ *  beta           in [0, 1); tau finite; patience >= 1.
+ *  stats          device [5] int32 counters of the step (decoupled_ppo_loss_fwd_bwd's
+ *                 stats_out), or NULL.
+ *  state          device pointer, 8-byte aligned (see dppo_ewma_state).
+ * n = 0 runs the controller only. The host checks the arguments above; w is checked on the
+ * device (state->error).
+ */
+dppo_status ewma_proxy_step(void* x_prox, const void* x_new, int32_t dtype, int64_t n,
+                            float beta, double tau, int32_t patience, int32_t normalized,
+                            const int32_t* stats, dppo_ewma_state* state, void* stream);
+
 /* Row-kernel policy, a testing and benchmarking hook: 0 = automatic (the
  * register-resident kernel when the row fits, the two-pass streaming kernel otherwise),
  * 1 = always the streaming kernel. Process-global; any other value is INVALID_ARG. */
@@ -278,7 +322,7 @@ const char* dppo_strerror(dppo_status s);
 const char* dppo_last_error(void);
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define DPPO_ABI_VERSION 2
+#define DPPO_ABI_VERSION 3
 int32_t dppo_abi_version(void);
 
 /*

@@ -25,7 +25,7 @@ __all__ = [
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
     "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
     "fused_lm_head_loss_fwd_bwd", "LmHeadResult", "lm_head_workspace_bytes",
-    "logprob_fwd_versioned",
+    "logprob_fwd_versioned", "EwmaProxyDevice",
 ]
 
 
@@ -367,6 +367,70 @@ class EwmaProxy:
     def load_state_dict(self, sd):
         self.x.copy_(sd["x"])
         for k in ("w", "streak", "resets", "beta", "tau", "patience", "normalized"):
+            setattr(self, k, sd[k])
+
+
+class EwmaProxyDevice:
+    """PPO-EWMA reference with automatic reset, both on the device (Sec. 5.2; App. B;
+    App. E): `step(x_new, stats)` takes the loss stage's stats tensor as it lies in device
+    memory and enqueues the reset rule and the update on the stream, with no
+    device-to-host copy and no synchronisation. The decisions and the buffer are those of
+    EwmaProxy; `read_state()` copies the 40-byte state to the host (one synchronisation).
+    """
+
+    STATE_BYTES = C.sizeof(_lib.DppoEwmaState)
+
+    def __init__(self, x0: torch.Tensor, beta: float, tau: float = 0.9, patience: int = 1,
+                 normalized: bool = True, w0: float = 1.0):
+        if not 0.0 <= beta < 1.0:
+            raise ValueError("beta must lie in [0, 1)")
+        if not x0.is_cuda:
+            raise ValueError("the proxy buffer must be a GPU tensor")
+        self.x = x0.clone()
+        self.beta = float(beta)
+        self.tau = float(tau)
+        self.patience = int(patience)
+        self.normalized = normalized
+        # int64 storage keeps the 40-byte state 8-byte aligned
+        self.state = torch.zeros(self.STATE_BYTES // 8, dtype=torch.int64, device=x0.device)
+        self.write_state(w=w0)
+
+    def write_state(self, w: float, streak: int = 0, resets: int = 0):
+        st = _lib.DppoEwmaState(w=float(w), streak=int(streak), resets=int(resets))
+        host = torch.frombuffer(bytearray(C.string_at(C.addressof(st), self.STATE_BYTES)),
+                                dtype=torch.int64)
+        self.state.copy_(host)
+
+    def read_state(self) -> dict:
+        raw = self.state.cpu().numpy().tobytes()
+        st = _lib.DppoEwmaState.from_buffer_copy(raw)
+        return {k: getattr(st, k) for k, _ in _lib.DppoEwmaState._fields_ if k != "reserved"}
+
+    def step(self, x_new: torch.Tensor, stats: torch.Tensor = None):
+        if x_new.dtype != self.x.dtype or x_new.numel() != self.x.numel():
+            raise ValueError("x_new must match the proxy buffer's dtype and size")
+        if not (x_new.is_contiguous() and x_new.is_cuda):
+            raise ValueError("x_new must be a contiguous GPU tensor")
+        sp = None
+        if stats is not None:
+            if not (stats.is_cuda and stats.dtype == torch.int32 and stats.numel() >= _lib.N_STATS
+                    and stats.is_contiguous()):
+                raise ValueError("stats must be the loss stage's int32 device tensor")
+            sp = stats.data_ptr()
+        st = _lib.lib().ewma_proxy_step(self.x.data_ptr(), x_new.data_ptr(), _dtype_code(self.x),
+                                        self.x.numel(), self.beta, self.tau, self.patience,
+                                        int(bool(self.normalized)), sp, self.state.data_ptr(),
+                                        _stream(self.x.device))
+        _lib.check(st, "ewma_proxy_step")
+
+    def state_dict(self):
+        return dict(x=self.x, state=self.state.clone(), beta=self.beta, tau=self.tau,
+                    patience=self.patience, normalized=self.normalized)
+
+    def load_state_dict(self, sd):
+        self.x.copy_(sd["x"])
+        self.state.copy_(sd["state"])
+        for k in ("beta", "tau", "patience", "normalized"):
             setattr(self, k, sd[k])
 
 

@@ -21,7 +21,7 @@ STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
 MAX_VERSIONS = 8
 DTYPE_F32, DTYPE_BF16 = 0, 1
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 # Every function the header declares, with its C signature.
 VP, I32, I64, F32, F64 = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double
@@ -34,11 +34,19 @@ class DppoParams(C.Structure):
                 ("loss_scale", C.c_float), ("ref_mode", C.c_int32), ("alpha", C.c_float)]
 
 
+class DppoEwmaState(C.Structure):
+    """dppo_ewma_state: device-resident PPO-EWMA normaliser and reset-controller state."""
+    _fields_ = [("w", C.c_double), ("streak", C.c_int32), ("resets", C.c_int32),
+                ("last_reset", C.c_int32), ("error", C.c_int32), ("last_rho", C.c_float),
+                ("ca", C.c_float), ("cb", C.c_float), ("reserved", C.c_int32)]
+
+
 SIGNATURES = {
     "logprob_fwd": (I32, [VP, I32, I64, I64, I64, VP, VP, VP, VP]),
     "decoupled_ppo_loss_fwd_bwd": (I32, [VP, I32, I64, I64, I64, VP, VP, VP, VP, VP, VP,
                                          C.POINTER(DppoParams), VP, VP, VP, VP, VP, I64, VP, VP]),
     "ewma_proxy_update": (I32, [VP, VP, I32, I64, F32, C.POINTER(C.c_double), I32, I32, VP]),
+    "ewma_proxy_step": (I32, [VP, VP, I32, I64, F32, F64, I32, I32, VP, VP, VP]),
     "dppo_strerror": (C.c_char_p, [I32]),
     "dppo_last_error": (C.c_char_p, []),
     "dppo_abi_version": (I32, []),

@@ -620,4 +620,32 @@ dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, in
   return DPPO_OK;
 }
 
+dppo_status ewma_proxy_step(void* x_prox, const void* x_new, int32_t dtype, int64_t n,
+                            float beta, double tau, int32_t patience, int32_t normalized,
+                            const int32_t* stats, dppo_ewma_state* state, void* stream) {
+  if (dtype != DPPO_F32 && dtype != DPPO_BF16)
+    return fail(DPPO_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (n < 0) return fail(DPPO_ERR_INVALID_ARG, "n = %lld < 0", (long long)n);
+  if (!(beta >= 0.0f && beta < 1.0f)) return fail(DPPO_ERR_INVALID_ARG, "beta = %g not in [0, 1)", beta);
+  if (!std::isfinite(tau)) return fail(DPPO_ERR_INVALID_ARG, "tau = %g is not finite", tau);
+  if (patience < 1) return fail(DPPO_ERR_INVALID_ARG, "patience = %d < 1", (int)patience);
+  if (!state) return fail(DPPO_ERR_INVALID_ARG, "state is required");
+  if (reinterpret_cast<uintptr_t>(state) % 8 != 0)
+    return fail(DPPO_ERR_INVALID_ARG, "state must be 8-byte aligned");
+  if (n > 0 && (!x_prox || !x_new)) return fail(DPPO_ERR_INVALID_ARG, "x_prox and x_new are required");
+  const int es = esize_of(dtype);
+  if (n > 0 && x_prox != x_new &&
+      overlaps(span_of(x_prox, 1, n, n, es), span_of(x_new, 1, n, n, es)))
+    return fail(DPPO_ERR_INVALID_ARG, "x_prox overlaps x_new without aliasing them exactly");
+  if (n > 0 && (overlaps(span_of(state, 1, 1, 1, (int)sizeof(dppo_ewma_state)), span_of(x_prox, 1, n, n, es)) ||
+                overlaps(span_of(state, 1, 1, 1, (int)sizeof(dppo_ewma_state)), span_of(x_new, 1, n, n, es))))
+    return fail(DPPO_ERR_INVALID_ARG, "state overlaps x_prox or x_new");
+  const bool aligned = n > 0 && aligned16(x_prox) && aligned16(x_new);
+  const hipError_t e = dppo::launch_ewma_step(x_prox, x_new, dtype == DPPO_BF16, n, beta, tau,
+                                              patience, normalized != 0, stats, state, aligned,
+                                              (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "ewma step launch");
+  return DPPO_OK;
+}
+
 }  // extern "C"

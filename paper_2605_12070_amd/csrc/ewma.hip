@@ -1,6 +1,7 @@
 // PPO-EWMA proxy update on a flat buffer (Sec. 5.2, Eq. 5; App. B of arXiv 2605.12070):
-// x_prox <- a * x_new + b * x_prox with host-computed coefficients (a, b). b = 0 means the
-// old contents are not read (first step, reset). HBM-bound: one 16-byte vector per
+// x_prox <- a * x_new + b * x_prox, with the coefficients (a, b) computed on the host, or
+// on the device together with the reset rule of Sec. 5.2 (ewma_controller). b = 0 means
+// the old contents are not read (first step, reset). HBM-bound: one 16-byte vector per
 // thread, float32 arithmetic, bf16 storage rounded to nearest even.
 #include "dppo.h"
 #include "dppo_device.h"
@@ -8,27 +9,28 @@
 
 namespace dppo {
 
-template <bool BF16, bool READ_OLD>
-__global__ __launch_bounds__(256) void ewma_kernel(void* xp_, const void* xn_,
-                                                   int64_t n, float ca, float cb) {
+// x_prox <- ca x_new + cb x_prox for the 16-byte vector i (or, past the vectors, the tail
+// element it stands for); the old value is not read when read_old is false.
+template <bool BF16>
+__device__ __forceinline__ void ewma_vec(void* xp_, const void* xn_, int64_t n, int64_t i,
+                                         float ca, float cb, bool read_old) {
   constexpr int E = BF16 ? 8 : 4;  // elements per 16-byte vector
   const int64_t nvec = n / E;
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nvec) {
     u32x4* xp = (u32x4*)xp_;
     const u32x4 vn = __builtin_nontemporal_load((const u32x4*)xn_ + i);
     u32x4 vo = {0u, 0u, 0u, 0u};
-    if (READ_OLD) vo = xp[i];
+    if (read_old) vo = xp[i];
     u32x4 out;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (BF16) {
-        const float lo = READ_OLD ? __builtin_fmaf(cb, bf16_lo(vo[k]), ca * bf16_lo(vn[k])) : ca * bf16_lo(vn[k]);
-        const float hi = READ_OLD ? __builtin_fmaf(cb, bf16_hi(vo[k]), ca * bf16_hi(vn[k])) : ca * bf16_hi(vn[k]);
+        const float lo = read_old ? __builtin_fmaf(cb, bf16_lo(vo[k]), ca * bf16_lo(vn[k])) : ca * bf16_lo(vn[k]);
+        const float hi = read_old ? __builtin_fmaf(cb, bf16_hi(vo[k]), ca * bf16_hi(vn[k])) : ca * bf16_hi(vn[k]);
         out[k] = pack_bf16(lo, hi);
       } else {
         const float x = __uint_as_float(vn[k]);
-        const float r = READ_OLD ? __builtin_fmaf(cb, __uint_as_float(vo[k]), ca * x) : ca * x;
+        const float r = read_old ? __builtin_fmaf(cb, __uint_as_float(vo[k]), ca * x) : ca * x;
         out[k] = __float_as_uint(r);
       }
     }
@@ -41,31 +43,107 @@ __global__ __launch_bounds__(256) void ewma_kernel(void* xp_, const void* xn_,
   if (BF16) {
     uint16_t* p = (uint16_t*)xp_;
     const float xnew = bf16_to_f32(((const uint16_t*)xn_)[e]);
-    const float r = READ_OLD ? __builtin_fmaf(cb, bf16_to_f32(p[e]), ca * xnew) : ca * xnew;
+    const float r = read_old ? __builtin_fmaf(cb, bf16_to_f32(p[e]), ca * xnew) : ca * xnew;
     p[e] = to_bf16(r);
   } else {
     float* p = (float*)xp_;
     const float xnew = ((const float*)xn_)[e];
-    p[e] = READ_OLD ? __builtin_fmaf(cb, p[e], ca * xnew) : ca * xnew;
+    p[e] = read_old ? __builtin_fmaf(cb, p[e], ca * xnew) : ca * xnew;
   }
 }
 
-// Unaligned buffers: one element per thread.
+// Unaligned buffers: element e alone.
+template <bool BF16>
+__device__ __forceinline__ void ewma_elem(void* xp_, const void* xn_, int64_t e, float ca,
+                                          float cb, bool read_old) {
+  if (BF16) {
+    uint16_t* p = (uint16_t*)xp_;
+    const float xnew = bf16_to_f32(((const uint16_t*)xn_)[e]);
+    const float r = read_old ? __builtin_fmaf(cb, bf16_to_f32(p[e]), ca * xnew) : ca * xnew;
+    p[e] = to_bf16(r);
+  } else {
+    float* p = (float*)xp_;
+    const float xnew = ((const float*)xn_)[e];
+    p[e] = read_old ? __builtin_fmaf(cb, p[e], ca * xnew) : ca * xnew;
+  }
+}
+
+// Host-computed coefficients.
+template <bool BF16, bool READ_OLD>
+__global__ __launch_bounds__(256) void ewma_kernel(void* xp_, const void* xn_,
+                                                   int64_t n, float ca, float cb) {
+  ewma_vec<BF16>(xp_, xn_, n, (int64_t)blockIdx.x * blockDim.x + threadIdx.x, ca, cb, READ_OLD);
+}
+
 template <bool BF16, bool READ_OLD>
 __global__ __launch_bounds__(256) void ewma_kernel_scalar(void* xp_, const void* xn_, int64_t n,
                                                           float ca, float cb) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= n) return;
-  if (BF16) {
-    uint16_t* p = (uint16_t*)xp_;
-    const float xnew = bf16_to_f32(((const uint16_t*)xn_)[e]);
-    const float r = READ_OLD ? __builtin_fmaf(cb, bf16_to_f32(p[e]), ca * xnew) : ca * xnew;
-    p[e] = to_bf16(r);
-  } else {
-    float* p = (float*)xp_;
-    const float xnew = ((const float*)xn_)[e];
-    p[e] = READ_OLD ? __builtin_fmaf(cb, p[e], ca * xnew) : ca * xnew;
+  if (e < n) ewma_elem<BF16>(xp_, xn_, e, ca, cb, READ_OLD);
+}
+
+// Coefficients from the device-resident controller state (written by ewma_controller in
+// the preceding launch on the same stream); a step that flagged an error writes nothing.
+template <bool BF16>
+__global__ __launch_bounds__(256) void ewma_kernel_dev(void* xp_, const void* xn_, int64_t n,
+                                                       const dppo_ewma_state* s) {
+  if (s->error) return;
+  const float ca = s->ca, cb = s->cb;
+  ewma_vec<BF16>(xp_, xn_, n, (int64_t)blockIdx.x * blockDim.x + threadIdx.x, ca, cb, cb != 0.0f);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void ewma_kernel_scalar_dev(void* xp_, const void* xn_,
+                                                              int64_t n, const dppo_ewma_state* s) {
+  if (s->error) return;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const float ca = s->ca, cb = s->cb;
+  if (e < n) ewma_elem<BF16>(xp_, xn_, e, ca, cb, cb != 0.0f);
+}
+
+// The reset rule (Sec. 5.2, App. E) and the coefficients of the recursion (App. B), in
+// double as the host path computes them: one thread.
+__global__ __launch_bounds__(64) void ewma_controller(const int32_t* stats, dppo_ewma_state* s,
+                                                      float beta, double tau, int32_t patience,
+                                                      int32_t normalized) {
+  if (threadIdx.x != 0) return;
+  dppo_ewma_state st = *s;
+  if (normalized && !(__builtin_isfinite(st.w) && st.w >= 0.0)) {
+    s->error = 1;
+    return;
   }
+  double rho = 1.0;
+  bool fire = false;
+  if (stats != nullptr) {
+    const int32_t nv = stats[DPPO_STAT_N_VALID];
+    rho = nv == 0 ? 1.0 : (double)stats[DPPO_STAT_N_ACTIVE] / (double)nv;
+    st.streak = rho < tau ? st.streak + 1 : 0;
+    fire = st.streak >= patience;
+    if (fire) {
+      st.streak = 0;
+      st.resets += 1;
+    }
+  }
+  double ca, cb;
+  if (fire) {
+    ca = 1.0;
+    cb = 0.0;
+    if (normalized) st.w = 1.0;
+  } else if (normalized) {
+    const double wp = st.w;
+    st.w = 1.0 + (double)beta * wp;
+    ca = 1.0 / st.w;
+    cb = (double)beta * wp / st.w;
+  } else {
+    ca = 1.0 - (double)beta;
+    cb = (double)beta;
+  }
+  st.last_reset = fire ? 1 : 0;
+  st.error = 0;
+  st.last_rho = (float)rho;
+  st.ca = (float)ca;
+  st.cb = (float)cb;
+  *s = st;
 }
 
 hipError_t launch_ewma(void* xp, const void* xn, bool bf16, int64_t n, float ca, float cb,
@@ -94,6 +172,26 @@ hipError_t launch_ewma(void* xp, const void* xn, bool bf16, int64_t n, float ca,
       if (read_old) ewma_kernel_scalar<false, true><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
       else ewma_kernel_scalar<false, false><<<g, b, 0, st>>>(xp, xn, n, ca, cb);
     }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_ewma_step(void* xp, const void* xn, bool bf16, int64_t n, float beta,
+                            double tau, int32_t patience, bool normalized, const int32_t* stats,
+                            dppo_ewma_state* state, bool aligned, hipStream_t st) {
+  ewma_controller<<<1, 64, 0, st>>>(stats, state, beta, tau, patience, normalized ? 1 : 0);
+  if (n == 0) return hipGetLastError();
+  const int64_t E = aligned ? (bf16 ? 8 : 4) : 1;
+  const int64_t threads = n / E + n % E;
+  const int64_t blocks = (threads + 255) / 256;
+  if (blocks < 1 || blocks > 0x7fffffff) return hipErrorInvalidValue;
+  const dim3 g((unsigned)blocks), b(256);
+  if (aligned) {
+    if (bf16) ewma_kernel_dev<true><<<g, b, 0, st>>>(xp, xn, n, state);
+    else ewma_kernel_dev<false><<<g, b, 0, st>>>(xp, xn, n, state);
+  } else {
+    if (bf16) ewma_kernel_scalar_dev<true><<<g, b, 0, st>>>(xp, xn, n, state);
+    else ewma_kernel_scalar_dev<false><<<g, b, 0, st>>>(xp, xn, n, state);
   }
   return hipGetLastError();
 }

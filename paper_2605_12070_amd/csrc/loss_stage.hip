@@ -692,6 +692,7 @@ __global__ __launch_bounds__(1024) void prep_stats(const uint8_t* mask, int64_t 
 
 // L = sum_t m_t s_t l_t in float64, each thread over a fixed stride, then a fixed tree:
 // the same inputs give the same bits on every run.
+template <bool HAS_MASK, bool HAS_TSCALE>
 __global__ __launch_bounds__(1024) void loss_sum(const float* loss_tok, const uint8_t* mask,
                                                  const float* tscale, const int32_t* stats,
                                                  int64_t T, float loss_scale, int32_t scale_mode,
@@ -702,11 +703,24 @@ __global__ __launch_bounds__(1024) void loss_sum(const float* loss_tok, const ui
     const int n = stats[DPPO_STAT_N_VALID];
     scale = loss_scale / (float)(n > 1 ? n : 1);
   }
+  // Thread k adds tokens k, k + 1024, k + 2048, ... in that order; the loads of 16 of them
+  // are issued together so that their latencies overlap.
+  constexpr int U = 16;
   double acc = 0.0;
-  for (int64_t i = threadIdx.x; i < T; i += 1024) {
-    if (mask && mask[i] == 0) continue;
-    const float s = scale * (tscale ? tscale[i] : 1.0f);
-    acc += (double)s * (double)loss_tok[i];
+  for (int64_t base = threadIdx.x; base < T; base += 1024 * U) {
+    float lt[U], ts[U];
+    bool on[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + (int64_t)u * 1024;
+      const int64_t j = i < T ? i : T - 1;   // in bounds (T >= 1 here): loads without branches
+      lt[u] = loss_tok[j];
+      ts[u] = HAS_TSCALE ? tscale[j] : 1.0f;
+      on[u] = (i < T) & ((HAS_MASK ? mask[j] : (uint8_t)1) != 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (on[u]) acc += (double)(scale * ts[u]) * (double)lt[u];
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
@@ -824,7 +838,9 @@ void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream
 void launch_loss_sum(const float* loss_tok, const uint8_t* mask, const float* tscale,
                      const int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
                      float* loss_out, hipStream_t st) {
-  loss_sum<<<1, 1024, 0, st>>>(loss_tok, mask, tscale, stats, T, loss_scale, scale_mode, loss_out);
+  auto k = mask ? (tscale ? loss_sum<true, true> : loss_sum<true, false>)
+                : (tscale ? loss_sum<false, true> : loss_sum<false, false>);
+  k<<<1, 1024, 0, st>>>(loss_tok, mask, tscale, stats, T, loss_scale, scale_mode, loss_out);
 }
 
 }  // namespace dppo

@@ -150,6 +150,39 @@ def test_ewma_rejects_bad_arguments(kw, frag):
     assert frag in _lib.lib().dppo_last_error().decode()
 
 
+@pytest.mark.parametrize("kw,frag", [
+    (dict(dtype=3), "dtype"),
+    (dict(n=-1), "n ="),
+    (dict(beta=1.0), "beta"),
+    (dict(beta=float("nan")), "beta"),
+    (dict(tau=float("inf")), "tau"),
+    (dict(tau=float("nan")), "tau"),
+    (dict(patience=0), "patience"),
+    (dict(state=None), "state is required"),
+    (dict(state=FAKE + 65536 + 4), "8-byte aligned"),
+    (dict(xp=None), "required"),
+    (dict(xn=FAKE + 8), "overlaps"),
+    (dict(state=FAKE + 32), "state overlaps"),
+])
+def test_ewma_step_rejects_bad_arguments(kw, frag):
+    """The device-side step checks its host arguments before any launch (the normaliser
+    itself lives on the device and is checked there)."""
+    d = dict(xp=FAKE, xn=FAKE + 4096, dtype=0, n=16, beta=0.5, tau=0.9, patience=1,
+             normalized=1, stats=None, state=FAKE + 65536)
+    d.update(kw)
+    st = _lib.lib().ewma_proxy_step(d["xp"], d["xn"], d["dtype"], d["n"], d["beta"], d["tau"],
+                                    d["patience"], d["normalized"], d["stats"], d["state"], None)
+    assert st == _lib.DPPO_ERR_INVALID_ARG
+    assert frag in _lib.lib().dppo_last_error().decode()
+
+
+def test_ewma_state_layout():
+    """dppo_ewma_state is 40 bytes with the normaliser first (the binding writes it)."""
+    assert C.sizeof(_lib.DppoEwmaState) == 40
+    assert _lib.DppoEwmaState.w.offset == 0 and _lib.DppoEwmaState.last_rho.offset == 24
+    assert _lib.DppoEwmaState.cb.offset == 32
+
+
 def test_ewma_empty_buffer_updates_w_only():
     w = C.c_double(0.0)
     L = _lib.lib()
