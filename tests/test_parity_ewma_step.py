@@ -7,8 +7,9 @@ import torch
 
 import oracle
 import paper_2605_12070_amd as P
+from paper_2605_12070_amd import workloads as W
 
-from helpers import bits_of
+from helpers import bits_of, oracle_params, tie_mask
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -130,3 +131,77 @@ def test_device_step_unaligned_and_empty(dtype):
                torch.tensor(_stats_for(0.5), dtype=torch.int32, device=DEV))
     st = e.read_state()
     assert st["streak"] == 2 and st["resets"] == 0 and st["w"] == 1.0 + 0.5 * (1.0 + 0.5)
+
+
+def test_collapse_of_the_loss_stage_triggers_the_reset():
+    """End to end: the loss kernel's own counters drive both controllers. A healthy step,
+    then two steps where lp_mu is shifted by +1 on 30 % of the tokens (r_d = e^-1 < 0.5,
+    outside the band), then a healthy one. With patience 2 the reset fires on the second
+    collapsed step, exactly where the oracle's counters put it."""
+    T, V = 512, 4096
+    _say("collapse -> reset", T, V)
+    wl = W.make_workload("small_vocab", device=DEV, T=T, V=V)
+    zb = bits_of(wl.logits)
+    ids = wl.ids.cpu().numpy()
+    anchor, _ = oracle.logprob_fwd(zb, ids)
+    lp_ref, lp_mu = W.reference_logprobs(torch.from_numpy(anchor), wl)
+    g = np.random.default_rng(4)
+    shift = torch.zeros(T, device=DEV)
+    shift[torch.from_numpy(g.choice(T, size=int(0.3 * T), replace=False)).to(DEV)] = 1.0
+    plans = [0.0, 1.0, 1.0, 0.0]
+    x0 = torch.zeros(T, device=DEV)
+    dev_ctl = P.EwmaProxyDevice(x0, 0.75, tau=0.9, patience=2)
+    host_ctl = P.EwmaProxy(x0, 0.75, tau=0.9, patience=2)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    rhos, fired_dev, fired_host = [], [], []
+    for k, amount in enumerate(plans):
+        mu = (lp_mu + amount * shift).to(DEV)
+        ref = lp_ref.to(DEV)
+        out = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, mu, ref, wl.adv, wl.mask)
+        o = oracle.decoupled_ppo_loss(zb, ids, mu.cpu().double().numpy(), ref.cpu().double().numpy(),
+                                      wl.adv.cpu().double().numpy(), wl.mask.cpu().numpy(),
+                                      params=params, want_dlogits=False)
+        # counters agree exactly away from threshold ties (each tie may go either way)
+        n_ties = int(tie_mask(o, params).sum())
+        diff = np.abs(out.stats.cpu().numpy().astype(np.int64) - np.asarray(o["stats"], np.int64))
+        assert diff[0] == 0 and diff[4] == 0 and np.all(diff <= n_ties), (k, diff, n_ties)
+        rhos.append(oracle.train_infer_mask_value(out.stats.cpu().tolist()))
+        x_new = torch.full((T,), float(k + 1), device=DEV)
+        dev_ctl.step(x_new, out.stats)
+        fired_dev.append(bool(dev_ctl.read_state()["last_reset"]))
+        fired_host.append(host_ctl.step(x_new, out.stats))
+    assert rhos[0] >= 0.9 and rhos[1] < 0.9 and rhos[2] < 0.9 and rhos[3] >= 0.9, rhos
+    expect = oracle.reset_schedule(rhos, 0.9, 2)
+    assert expect == [False, False, True, False]
+    assert fired_dev == expect and fired_host == expect
+    assert torch.equal(dev_ctl.x, host_ctl.x)
+    assert dev_ctl.read_state()["w"] == host_ctl.w == 1.75
+
+
+@pytest.mark.parametrize("device_side", [True, False])
+def test_controller_checkpoint_resume(device_side):
+    """Saving the controller's state mid-run and loading it into a fresh controller gives
+    the same continuation, bit for bit (the state is the buffer plus a few scalars)."""
+    n = 1000
+    _say("checkpoint resume", device_side)
+    g = torch.Generator(device=DEV).manual_seed(21)
+    xs = [torch.randn(n, generator=g, device=DEV) for _ in range(7)]
+    stats = [torch.tensor(_stats_for(r), dtype=torch.int32, device=DEV)
+             for r in (0.95, 0.5, 0.95, 0.5, 0.5, 0.95, 0.5)]
+    mk = (lambda: P.EwmaProxyDevice(xs[0], 0.8, tau=0.9, patience=2)) if device_side else \
+         (lambda: P.EwmaProxy(xs[0], 0.8, tau=0.9, patience=2))
+    a = mk()
+    for t in range(3):
+        a.step(xs[t], stats[t])
+    saved = {k: (v.clone() if torch.is_tensor(v) else v) for k, v in a.state_dict().items()}
+    for t in range(3, 7):
+        a.step(xs[t], stats[t])
+    b = mk()
+    b.load_state_dict(saved)
+    for t in range(3, 7):
+        b.step(xs[t], stats[t])
+    assert torch.equal(a.x, b.x)
+    if device_side:
+        assert a.read_state() == b.read_state()
+    else:
+        assert (a.w, a.streak, a.resets) == (b.w, b.streak, b.resets)
