@@ -196,6 +196,61 @@ def versioned_logprob_measure(dev, wl, K=4, reps=20):
             "tokens_per_s": round(T / (call_ms * 1e-3), 1)}
 
 
+def vocab_shard_measure(dev, wl, lp_mu, lp_ref, n_shards=8, reps=20):
+    """One GPU's share of an n_shards-way vocabulary-parallel loss stage on the large_vocab batch:
+    a contiguous [T, V / n_shards] bf16 shard. Times the shard-statistics kernel (reads the shard) and
+    the shard loss kernel (reads it again, writes its dlogits); the exchange between shards
+    is not part of a one-GPU run. The global lse and z[y] come from the unsharded log-prob
+    call (input preparation, not timed)."""
+    T, V = wl.T, wl.V
+    Vs = V // n_shards
+    shard = wl.logits[:, :Vs].contiguous()
+    dl = torch.empty_like(shard)
+    lp, lse = P.logprob_fwd(wl.logits, wl.ids, with_lse=True)
+    zy = lp + lse
+    kw = dict(scale_mode="const", loss_scale=1.0)
+
+    def stats():
+        return P.vocab_shard_stats(shard, wl.ids, 0, V, wl.mask)
+
+    def loss():
+        return P.decoupled_ppo_loss_shard_fwd_bwd(shard, 0, V, lse, zy, wl.ids, lp_mu, lp_ref,
+                                                   wl.adv, wl.mask, dlogits=dl, **kw)
+
+    res = {}
+    for name, fn in (("stats", stats), ("loss", loss)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with P.KernelTimer() as kt:
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            k_ms, k_n = kt.read()
+        res[name] = (k_ms / max(1, k_n), e0.elapsed_time(e1) / reps)
+    n_valid = int(wl.mask.sum().item())
+    b_stats = n_valid * Vs * 2 + T * (8 + 1 + 4 + 4)
+    b_loss = n_valid * Vs * 2 + T * Vs * 2 + T * (30 + 8)
+    k_stats, c_stats = res["stats"]
+    k_loss, c_loss = res["loss"]
+    ach = b_loss / (k_loss * 1e-3) / 1e9
+    del shard, dl
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBPS, 4), "kernel": "dppo::shard_loss<true, true>",
+            "kernel_ms": round(k_loss, 4), "alg_bytes_per_launch": b_loss,
+            "shard": f"T={T} x Vs={Vs} (V/{n_shards}) bf16, contiguous",
+            "stats_kernel": {"kernel": "dppo::shard_stats<true, true>",
+                             "kernel_ms": round(k_stats, 4), "alg_bytes_per_launch": b_stats,
+                             "achieved": round(b_stats / (k_stats * 1e-3) / 1e9, 1),
+                             "frac": round(b_stats / (k_stats * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
+            "step_ms": round(c_stats + c_loss, 4),
+            "tokens_per_s": round(T / ((c_stats + c_loss) * 1e-3), 1)}
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, AMD specification
 
 
@@ -256,6 +311,8 @@ def main():
                     help="size of the parameter-sized EWMA measurement (0 to skip)")
     ap.add_argument("--no-lm-head", action="store_true",
                     help="skip the fused LM-head measurement")
+    ap.add_argument("--no-shard", action="store_true",
+                    help="skip the vocabulary-shard measurement")
     ap.add_argument("--no-versioned", action="store_true",
                     help="skip the versioned log-prob measurement")
     args = ap.parse_args()
@@ -340,6 +397,9 @@ def main():
         "hbm_pct_of_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "roofline": roofline,
     }
+    if not args.no_shard and args.workload == "large_vocab":
+        log("vocabulary shard")
+        result["vocab_shard_roofline"] = vocab_shard_measure(dev, wl, lp_mu, lp_ref)
     if not args.no_versioned:
         log("versioned log-prob")
         del dlogits

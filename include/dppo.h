@@ -245,6 +245,67 @@ dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, in
                               void* stream);
 
 /*
+ * Vocabulary shards. The training engine's LM head may split the vocabulary over GPUs
+ * (tensor parallelism, one of the training-side implementations Sec. 1 names). A GPU then
+ * holds the column block [vocab_start, vocab_start + Vs) of the logits, and the per-token
+ * log-prob of Sec. 3.2 needs a log-sum-exp over every shard. The three calls below are one
+ * GPU's share of that path, at the shard's own shape:
+ *   1. vocab_shard_stats on every shard: the shard's row log-sum-exp and z[y] where it
+ *      holds column y;
+ *   2. an exchange across the shards, done by the caller: all-gather of shard_lse into
+ *      [P, T] (shard order), all-reduce sum of shard_zy (exactly one shard holds z[y]);
+ *      then vocab_shard_combine on every shard, which gives the same lse everywhere;
+ *   3. decoupled_ppo_loss_shard_fwd_bwd on every shard: the token math of Eq. 1-4 from
+ *      the global lse and z[y] (every shard computes the same per-token outputs, loss and
+ *      stats), and the shard's own columns of dlogits = w (softmax - onehot).
+ * With P = 1 and vocab_start = 0 the three calls compute decoupled_ppo_loss_fwd_bwd (up to
+ * rounding: the logits are read twice, not once).
+ */
+
+/*
+ * vocab_shard_stats -- per row t of a shard [T, Vs] (row stride ld elements):
+ *    shard_lse[t] = log sum_{v < Vs} exp z[t, v]   (-inf when every entry is -inf),
+ *    shard_zy[t]  = z[t, y_t - vocab_start] if vocab_start <= y_t < vocab_start + Vs, else 0.
+ *  Rows with loss_mask = 0 (nullable: all valid) are not read: shard_lse = -inf, shard_zy = 0.
+ *  V is the whole vocabulary: vocab_start >= 0 and vocab_start + Vs <= V, else INVALID_ARG.
+ *  NaN or +inf entries make shard_lse NaN.
+ */
+dppo_status vocab_shard_stats(const void* logits_shard, int32_t dtype, int64_t T, int64_t Vs,
+                              int64_t ld, int64_t vocab_start, int64_t V,
+                              const int64_t* token_ids, const uint8_t* loss_mask,
+                              float* shard_lse, float* shard_zy, void* stream);
+
+/*
+ * vocab_shard_combine -- lse[t] = log sum_p exp shard_lse[p][t] over P gathered shard
+ * statistics ([P, T] float32, shard-major), summed in shard order around their maximum.
+ * A token whose shards are all -inf (its row masked, or all of its logits -inf) gets NaN,
+ * as the unsharded log-sum-exp gives for a row of -inf. lse may not overlap shard_lse.
+ */
+dppo_status vocab_shard_combine(const float* shard_lse, int32_t P, int64_t T, float* lse,
+                                void* stream);
+
+/*
+ * decoupled_ppo_loss_shard_fwd_bwd -- decoupled_ppo_loss_fwd_bwd on one shard, with the row
+ * statistics given: lp = zy - lse per token, then the ratios, band, PPO clip, loss and MIS
+ * weight w exactly as decoupled_ppo_loss_fwd_bwd computes them (Eq. 1-4, Sec. 3.1), and
+ *    dlogits_shard[t, v] = w_t (exp(z[t, v] - lse_t) - 1{vocab_start + v = y_t}),  v < Vs.
+ *  lse, zy      [T] float32: vocab_shard_combine's lse and the all-reduced shard_zy.
+ *  token_ids    global ids; y outside [0, V) is a bad id (lp NaN, loss 0, a zero gradient
+ *               row, stats[4]++), as in decoupled_ppo_loss_fwd_bwd.
+ *  Every other argument, output, alias rule (dlogits_shard may be logits_shard with the same
+ *  stride) and error convention is that of decoupled_ppo_loss_fwd_bwd with V replaced by Vs
+ *  for the matrices. The per-token outputs, loss and stats are the same on every shard:
+ *  they are not to be summed across shards.
+ */
+dppo_status decoupled_ppo_loss_shard_fwd_bwd(
+    const void* logits_shard, int32_t dtype, int64_t T, int64_t Vs, int64_t ld,
+    int64_t vocab_start, int64_t V, const int64_t* token_ids, const float* lse, const float* zy,
+    const float* logp_mu_old, const float* logp_ref, const float* advantages,
+    const uint8_t* loss_mask, const float* token_scale, const dppo_params* p, float* logp_out,
+    float* loss_tok_out, float* loss_out, uint8_t* flags_out, void* dlogits_shard,
+    int64_t ld_dlogits, int32_t* stats_out, void* stream);
+
+/*
  * Device-resident state of the PPO-EWMA reference and of its automatic reset (Sec. 5.2,
  * App. B, App. E), for ewma_proxy_step. 40 bytes, 8-byte aligned, in device memory owned by
  * the caller; checkpoint it together with the proxy buffer. Initialise with the host: w as
@@ -322,13 +383,14 @@ const char* dppo_strerror(dppo_status s);
 const char* dppo_last_error(void);
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define DPPO_ABI_VERSION 3
+#define DPPO_ABI_VERSION 4
 int32_t dppo_abi_version(void);
 
 /*
  * Kernel timer for profiling. While enabled, the library records a pair of HIP events on
  * the call's stream around every launch of the per-row loss-stage kernel (the one that
- * streams the logits) and, on dppo_timer_read, synchronises those events and returns the
+ * streams the logits; for the vocabulary-shard calls, the shard kernel; for the fused LM
+ * head, its two tile kernels) and, on dppo_timer_read, synchronises those events and returns the
  * summed elapsed time in milliseconds and the number of launches timed, then clears the
  * record. Enabling allocates host-side event objects; it is process-global state, meant
  * for one profiling thread.

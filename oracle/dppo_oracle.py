@@ -210,6 +210,38 @@ def batch_scale(mask, params: Params) -> float:
 # ---------------------------------------------------------------------------------------
 # The fused stage: forward values, MIS weights and dlogits
 # ---------------------------------------------------------------------------------------
+def token_terms(lp, valid, good, lp_mu, lp_ref, adv, ts, params: Params, scale: float):
+    """Everything the objective derives from a token's log-prob (float64 arrays [n]).
+
+    Ratios (Eq. 1), band (Eq. 4) and PPO (Eq. 3) decisions, the per-token loss (Eq. 2), the
+    MIS weight of the Sec. 3.1 gradient and the flags. Rows that are not valid, or whose id
+    is out of range, carry no loss, no weight and no decision bits.
+    """
+    ev = valid & good
+    r_s, r_d, _ = ratios(lp, lp_ref, lp_mu)
+    band = band_mask(r_d, params.band_lo, params.band_hi) & ev
+    ppo = ppo_active_mask(r_s, adv, params.clip_eps_lo, params.clip_eps_hi) & ev
+    uses_mask = params.rd_mode in ("mask", "mask_weight")
+    gate = ppo & (band if uses_mask else ev)
+    wd = discrepancy_weight(r_d, band, params.rd_mode)
+
+    with np.errstate(invalid="ignore", over="ignore"):
+        sur = clipped_surrogate(r_s, adv, params.clip_eps_lo, params.clip_eps_hi)
+        loss_tok = np.where(ev, -wd * sur, 0.0)
+        s = scale * ts
+        # MIS gradient form (Sec. 3.1) with r = r_d r_s: d(loss)/d(lp_theta) = -s wd r_s A
+        # on active tokens, 0 elsewhere.
+        w = np.where(gate, s * wd * r_s * adv, 0.0)
+
+    flags = np.zeros(len(lp), np.uint8)
+    flags[valid] |= FLAG_VALID
+    flags[valid & ~good] |= FLAG_BAD_ID
+    flags[band] |= FLAG_BAND
+    flags[ppo] |= FLAG_PPO
+    return dict(r_s=r_s, r_d=r_d, band=band, ppo=ppo, gate=gate, loss_tok=loss_tok, w=w, s=s,
+                flags=flags)
+
+
 def per_token(z, ids, lp_mu, lp_ref, adv, mask, token_scale, params: Params, scale: float,
               want_dlogits: bool = True):
     """Evaluate the decoupled MIS objective on a block of rows (float64).
@@ -236,29 +268,9 @@ def per_token(z, ids, lp_mu, lp_ref, adv, mask, token_scale, params: Params, sca
         lse[vr] = row_logsumexp(z[vr])
         lp[vr] = token_logprob(z[vr], ids[vr], lse[vr])
 
-    r_s, r_d, _ = ratios(lp, lp_ref, lp_mu)
-    band = band_mask(r_d, params.band_lo, params.band_hi) & ev
-    ppo = ppo_active_mask(r_s, adv, params.clip_eps_lo, params.clip_eps_hi) & ev
-    uses_mask = params.rd_mode in ("mask", "mask_weight")
-    gate = ppo & (band if uses_mask else ev)
-    wd = discrepancy_weight(r_d, band, params.rd_mode)
-
-    with np.errstate(invalid="ignore", over="ignore"):
-        sur = clipped_surrogate(r_s, adv, params.clip_eps_lo, params.clip_eps_hi)
-        loss_tok = np.where(ev, -wd * sur, 0.0)
-        s = scale * ts
-        # MIS gradient form (Sec. 3.1) with r = r_d r_s: d(loss)/d(lp_theta) = -s wd r_s A
-        # on active tokens, 0 elsewhere.
-        w = np.where(gate, s * wd * r_s * adv, 0.0)
-
-    flags = np.zeros(n, np.uint8)
-    flags[valid] |= FLAG_VALID
-    flags[valid & ~good] |= FLAG_BAD_ID
-    flags[band] |= FLAG_BAND
-    flags[ppo] |= FLAG_PPO
-
-    out = dict(lp=np.where(valid, lp, 0.0), lse=lse, r_s=r_s, r_d=r_d, band=band, ppo=ppo,
-               gate=gate, loss_tok=loss_tok, w=w, s=s, flags=flags, valid=valid, good=good)
+    out = token_terms(lp, valid, good, lp_mu, lp_ref, adv, ts, params, scale)
+    out.update(lp=np.where(valid, lp, 0.0), lse=lse, valid=valid, good=good)
+    w = out["w"]
     if want_dlogits:
         d = np.zeros((n, V))
         er = np.nonzero(ev)[0]
@@ -320,6 +332,74 @@ def decoupled_ppo_loss(logits, ids, lp_mu, lp_ref, adv, mask=None, token_scale=N
         out["loss"] = float(np.sum(np.where(valid, out["s"] * out["loss_tok"], 0.0)))
     out["stats"] = stats_of(out["flags"], params)
     out["scale"] = scale
+    return out
+
+
+# ---------------------------------------------------------------------------------------
+# Vocabulary shards: the same stage when the vocabulary columns are split over devices
+# ---------------------------------------------------------------------------------------
+def vocab_shard_stats(z_shard, ids, vocab_start, mask=None):
+    """One shard's row statistics: (lse_s, zy_s) float64 [n].
+
+    lse_s = log sum over the shard's columns of exp z (-inf for a shard of -inf only, which
+    then adds nothing to the global sum); zy_s = z[y] where the shard holds column y, else 0.
+    Rows with m = 0 are not evaluated: lse_s = -inf, zy_s = 0.
+    """
+    z = as_f64(z_shard)
+    n, Vs = z.shape
+    ids = np.asarray(ids, dtype=np.int64)
+    valid = np.ones(n, bool) if mask is None else (np.asarray(mask) != 0)
+    lse = np.full(n, -np.inf)
+    zy = np.zeros(n)
+    vr = np.nonzero(valid)[0]
+    if vr.size and Vs:
+        all_neg_inf = np.all(z[vr] == -np.inf, axis=1)
+        lse[vr] = np.where(all_neg_inf, -np.inf, row_logsumexp(z[vr]))
+    yl = ids - vocab_start
+    own = np.nonzero(valid & (yl >= 0) & (yl < Vs))[0]
+    zy[own] = z[own, yl[own]]
+    return lse, zy
+
+
+def vocab_shard_combine(shard_lse):
+    """Global lse = log sum_p exp lse_p over the shards ([P, n]); NaN where every shard is
+    -inf (a row of -inf logits, as row_logsumexp gives, or a masked row)."""
+    l = np.asarray(shard_lse, dtype=np.float64)
+    with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
+        m = np.max(l, axis=0)
+        out = m + np.log(np.sum(np.exp(l - m[None]), axis=0))
+    return np.where(m == -np.inf, np.nan, out)
+
+
+def vocab_shard_loss(z_shard, ids, vocab_start, V, lse, zy, lp_mu, lp_ref, adv, mask,
+                     token_scale, params: Params, scale: float, want_dlogits: bool = True):
+    """The loss stage on one shard given the global lse and z[y]: lp = z[y] - lse and the
+    token terms as in per_token; dlogits for the shard's columns v (global v + vocab_start):
+    w (exp(z - lse) - 1{v + vocab_start = y})."""
+    z = as_f64(z_shard)
+    n, Vs = z.shape
+    ids = np.asarray(ids, dtype=np.int64)
+    valid = np.ones(n, bool) if mask is None else (np.asarray(mask) != 0)
+    good = (ids >= 0) & (ids < V)
+    ts = np.ones(n) if token_scale is None else as_f64(token_scale)
+    lse = as_f64(lse)
+    lp = np.full(n, np.nan)
+    ev = valid & good
+    lp[ev] = as_f64(zy)[ev] - lse[ev]
+    out = token_terms(lp, valid, good, as_f64(lp_mu), as_f64(lp_ref), as_f64(adv), ts, params,
+                      scale)
+    out.update(lp=np.where(valid, lp, 0.0), lse=lse, valid=valid, good=good)
+    if want_dlogits:
+        w = out["w"]
+        d = np.zeros((n, Vs))
+        er = np.nonzero(ev)[0]
+        if er.size:
+            with np.errstate(invalid="ignore", over="ignore"):
+                d[er] = w[er, None] * np.exp(z[er] - lse[er, None])
+            yl = ids[er] - vocab_start
+            own = (yl >= 0) & (yl < Vs)
+            d[er[own], yl[own]] -= w[er[own]]
+        out["dlogits"] = d
     return out
 
 

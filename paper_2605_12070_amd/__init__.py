@@ -25,7 +25,8 @@ __all__ = [
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
     "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
     "fused_lm_head_loss_fwd_bwd", "LmHeadResult", "lm_head_workspace_bytes",
-    "logprob_fwd_versioned", "EwmaProxyDevice",
+    "logprob_fwd_versioned", "EwmaProxyDevice", "vocab_shard_stats", "vocab_shard_combine",
+    "decoupled_ppo_loss_shard_fwd_bwd",
 ]
 
 
@@ -158,6 +159,88 @@ def decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advanta
         out.flags.data_ptr() if out.flags is not None else None, d_ptr, ldd,
         out.stats.data_ptr(), _stream(dev))
     _lib.check(st, "decoupled_ppo_loss_fwd_bwd")
+    return out
+
+
+def vocab_shard_stats(logits_shard, token_ids, vocab_start: int, vocab_size: int,
+                      loss_mask=None):
+    """One vocabulary shard's row statistics: (shard_lse [T], shard_zy [T]) float32, the
+    log-sum-exp over the shard's columns and z[y] where the shard holds column y (0 else).
+    logits_shard [T, Vs] holds columns [vocab_start, vocab_start + Vs) of a vocab_size-
+    column vocabulary."""
+    ptr, T, Vs, ld = _matrix(logits_shard, "logits_shard")
+    dev = logits_shard.device
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    msk = _vec(loss_mask, T, torch.uint8, "loss_mask", dev, optional=True)
+    lse = torch.empty(T, dtype=torch.float32, device=dev)
+    zy = torch.empty(T, dtype=torch.float32, device=dev)
+    st = _lib.lib().vocab_shard_stats(ptr, _dtype_code(logits_shard), T, Vs, ld, int(vocab_start),
+                                      int(vocab_size), ids, msk, lse.data_ptr(), zy.data_ptr(),
+                                      _stream(dev))
+    _lib.check(st, "vocab_shard_stats")
+    return lse, zy
+
+
+def vocab_shard_combine(shard_lse: torch.Tensor) -> torch.Tensor:
+    """Global per-token log-sum-exp from the gathered shard statistics [P, T] (shard order)."""
+    if not (shard_lse.is_cuda and shard_lse.dtype == torch.float32 and shard_lse.dim() == 2
+            and shard_lse.is_contiguous()):
+        raise ValueError("shard_lse must be a contiguous [P, T] float32 GPU tensor")
+    P, T = shard_lse.shape
+    lse = torch.empty(T, dtype=torch.float32, device=shard_lse.device)
+    st = _lib.lib().vocab_shard_combine(shard_lse.data_ptr(), P, T, lse.data_ptr(),
+                                        _stream(shard_lse.device))
+    _lib.check(st, "vocab_shard_combine")
+    return lse
+
+
+def decoupled_ppo_loss_shard_fwd_bwd(logits_shard, vocab_start: int, vocab_size: int, lse, zy,
+                                     token_ids, logp_mu_old, logp_ref, advantages,
+                                     loss_mask=None, token_scale=None, *, band=(0.5, 2.0),
+                                     clip_eps=(0.2, 0.2), rd_mode="mask_weight",
+                                     scale_mode="token_mean", loss_scale=1.0, ref_mode="given",
+                                     alpha=0.5, want_dlogits=True, dlogits=None,
+                                     want_flags=True) -> LossResult:
+    """decoupled_ppo_loss_fwd_bwd on one vocabulary shard, from the global lse and z[y]
+    (vocab_shard_combine's lse, the all-reduced shard_zy): the per-token outputs, loss and
+    stats (the same on every shard) and this shard's columns of dlogits."""
+    ptr, T, Vs, ld = _matrix(logits_shard, "logits_shard")
+    dev = logits_shard.device
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    lse_p = _vec(lse, T, torch.float32, "lse", dev)
+    zy_p = _vec(zy, T, torch.float32, "zy", dev)
+    mu = _vec(logp_mu_old, T, torch.float32, "logp_mu_old", dev)
+    if ref_mode not in REF_MODES:
+        raise ValueError(f"ref_mode in {list(REF_MODES)}")
+    ref = _vec(logp_ref, T, torch.float32, "logp_ref", dev, optional=ref_mode != "given")
+    adv = _vec(advantages, T, torch.float32, "advantages", dev)
+    msk = _vec(loss_mask, T, torch.uint8, "loss_mask", dev, optional=True)
+    tsc = _vec(token_scale, T, torch.float32, "token_scale", dev, optional=True)
+    if rd_mode not in RD_MODES or scale_mode not in SCALE_MODES:
+        raise ValueError(f"rd_mode in {list(RD_MODES)}, scale_mode in {list(SCALE_MODES)}")
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = LossResult(
+        loss=torch.empty(1, **f32), logp=torch.empty(T, **f32), loss_tok=torch.empty(T, **f32),
+        flags=torch.empty(T, dtype=torch.uint8, device=dev) if want_flags else None,
+        stats=torch.empty(_lib.N_STATS, dtype=torch.int32, device=dev), dlogits=None)
+    d_ptr, ldd = None, 0
+    if want_dlogits:
+        if dlogits is None:
+            dlogits = torch.empty_like(logits_shard)
+        if (dlogits.dtype != logits_shard.dtype or dlogits.shape != logits_shard.shape
+                or dlogits.stride(1) != 1):
+            raise ValueError("dlogits must match logits_shard in dtype and shape, unit last stride")
+        out.dlogits = dlogits
+        d_ptr, ldd = dlogits.data_ptr(), dlogits.stride(0)
+    p = _lib.DppoParams(float(band[0]), float(band[1]), float(clip_eps[0]), float(clip_eps[1]),
+                        RD_MODES[rd_mode], SCALE_MODES[scale_mode], float(loss_scale),
+                        REF_MODES[ref_mode], float(alpha))
+    st = _lib.lib().decoupled_ppo_loss_shard_fwd_bwd(
+        ptr, _dtype_code(logits_shard), T, Vs, ld, int(vocab_start), int(vocab_size), ids, lse_p,
+        zy_p, mu, ref, adv, msk, tsc, C.byref(p), out.logp.data_ptr(), out.loss_tok.data_ptr(),
+        out.loss.data_ptr(), out.flags.data_ptr() if out.flags is not None else None, d_ptr, ldd,
+        out.stats.data_ptr(), _stream(dev))
+    _lib.check(st, "decoupled_ppo_loss_shard_fwd_bwd")
     return out
 
 

@@ -21,7 +21,7 @@ STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
 MAX_VERSIONS = 8
 DTYPE_F32, DTYPE_BF16 = 0, 1
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 # Every function the header declares, with its C signature.
 VP, I32, I64, F32, F64 = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double
@@ -47,6 +47,11 @@ SIGNATURES = {
                                          C.POINTER(DppoParams), VP, VP, VP, VP, VP, I64, VP, VP]),
     "ewma_proxy_update": (I32, [VP, VP, I32, I64, F32, C.POINTER(C.c_double), I32, I32, VP]),
     "ewma_proxy_step": (I32, [VP, VP, I32, I64, F32, F64, I32, I32, VP, VP, VP]),
+    "vocab_shard_stats": (I32, [VP, I32, I64, I64, I64, I64, I64, VP, VP, VP, VP, VP]),
+    "vocab_shard_combine": (I32, [VP, I32, I64, VP, VP]),
+    "decoupled_ppo_loss_shard_fwd_bwd": (I32, [VP, I32, I64, I64, I64, I64, I64, VP, VP, VP, VP, VP,
+                                               VP, VP, VP, C.POINTER(DppoParams), VP, VP, VP, VP,
+                                               VP, I64, VP, VP]),
     "dppo_strerror": (C.c_char_p, [I32]),
     "dppo_last_error": (C.c_char_p, []),
     "dppo_abi_version": (I32, []),

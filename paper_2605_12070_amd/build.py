@@ -21,7 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdppo.so")
-SOURCES = ["loss_stage.hip", "lm_head.hip", "ewma.hip", "abi.hip"]
+SOURCES = ["loss_stage.hip", "lm_head.hip", "ewma.hip", "vocab_shard.hip", "abi.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -13,6 +13,7 @@
 #include "dppo.h"
 #include "ewma.h"
 #include "lm_head.h"
+#include "vocab_shard.h"
 #include "loss_stage.h"
 
 #include <rocblas/rocblas.h>
@@ -645,6 +646,140 @@ dppo_status ewma_proxy_step(void* x_prox, const void* x_new, int32_t dtype, int6
                                               patience, normalized != 0, stats, state, aligned,
                                               (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "ewma step launch");
+  return DPPO_OK;
+}
+
+// ------------------------------------------------------------------ vocabulary shards
+namespace {
+// Shard geometry shared by the two per-row shard calls: columns [vstart, vstart + Vs) of a
+// V-column vocabulary, with 16-byte offsets inside one row kept within int range.
+dppo_status check_shard(const void* logits, int32_t dtype, int64_t T, int64_t Vs, int64_t ld,
+                        int64_t vstart, int64_t V) {
+  dppo_status s = check_matrix(logits, dtype, T, Vs, ld, "logits_shard");
+  if (s != DPPO_OK) return s;
+  if (Vs * esize_of(dtype) > (int64_t)1 << 30)
+    return fail(DPPO_ERR_INVALID_ARG, "shard row of %lld elements exceeds 1 GiB", (long long)Vs);
+  if (vstart < 0 || V < 1 || vstart + Vs > V)
+    return fail(DPPO_ERR_INVALID_ARG, "shard columns [%lld, %lld) outside [0, V = %lld)",
+                (long long)vstart, (long long)(vstart + Vs), (long long)V);
+  return DPPO_OK;
+}
+}  // namespace
+
+dppo_status vocab_shard_stats(const void* logits_shard, int32_t dtype, int64_t T, int64_t Vs,
+                              int64_t ld, int64_t vocab_start, int64_t V,
+                              const int64_t* token_ids, const uint8_t* loss_mask,
+                              float* shard_lse, float* shard_zy, void* stream) {
+  dppo_status s = check_shard(logits_shard, dtype, T, Vs, ld, vocab_start, V);
+  if (s != DPPO_OK) return s;
+  if (T > 0 && (!token_ids || !shard_lse || !shard_zy))
+    return fail(DPPO_ERR_INVALID_ARG, "token_ids, shard_lse and shard_zy are required");
+  if (T == 0) return DPPO_OK;
+  const int es = esize_of(dtype);
+  dppo::ShardArgs a{};
+  a.a.logits = logits_shard;
+  a.a.ld = ld;
+  a.a.ids = token_ids;
+  a.a.mask = loss_mask;
+  a.a.T = (int32_t)T;
+  a.a.V = (int32_t)Vs;
+  a.vstart = vocab_start;
+  a.vtot = V;
+  a.lse_out = shard_lse;
+  a.zy_out = shard_zy;
+  const bool vec = aligned16(logits_shard) && (ld * es) % 16 == 0;
+  auto* ev = timer_slot();
+  if (ev) (void)hipEventRecord(ev->first, (hipStream_t)stream);
+  const hipError_t e = dppo::launch_shard_stats(a, dtype == DPPO_BF16, vec, (hipStream_t)stream);
+  if (ev) (void)hipEventRecord(ev->second, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "shard stats launch");
+  return DPPO_OK;
+}
+
+dppo_status vocab_shard_combine(const float* shard_lse, int32_t P, int64_t T, float* lse,
+                                void* stream) {
+  if (P < 1) return fail(DPPO_ERR_INVALID_ARG, "P = %d shards < 1", (int)P);
+  if (T < 0 || T > 0x7FFFFFFF) return fail(DPPO_ERR_INVALID_ARG, "T = %lld out of [0, 2^31)", (long long)T);
+  if (T > 0 && (!shard_lse || !lse)) return fail(DPPO_ERR_INVALID_ARG, "shard_lse and lse are required");
+  if (T > 0 && overlaps(span_of(shard_lse, P, T, T, 4), span_of(lse, 1, T, T, 4)))
+    return fail(DPPO_ERR_INVALID_ARG, "lse overlaps shard_lse");
+  if (T == 0) return DPPO_OK;
+  const hipError_t e = dppo::launch_shard_combine(shard_lse, P, T, lse, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "shard combine launch");
+  return DPPO_OK;
+}
+
+dppo_status decoupled_ppo_loss_shard_fwd_bwd(
+    const void* logits_shard, int32_t dtype, int64_t T, int64_t Vs, int64_t ld,
+    int64_t vocab_start, int64_t V, const int64_t* token_ids, const float* lse, const float* zy,
+    const float* logp_mu_old, const float* logp_ref, const float* advantages,
+    const uint8_t* loss_mask, const float* token_scale, const dppo_params* p, float* logp_out,
+    float* loss_tok_out, float* loss_out, uint8_t* flags_out, void* dlogits_shard,
+    int64_t ld_dlogits, int32_t* stats_out, void* stream) {
+  dppo_status s = check_shard(logits_shard, dtype, T, Vs, ld, vocab_start, V);
+  if (s != DPPO_OK) return s;
+  if (!p) return fail(DPPO_ERR_INVALID_ARG, "params pointer is NULL");
+  if (!loss_out || !stats_out) return fail(DPPO_ERR_INVALID_ARG, "loss_out and stats_out are required");
+  s = check_token_args(p, T, token_ids, logp_mu_old, logp_ref, advantages, logp_out, loss_tok_out);
+  if (s != DPPO_OK) return s;
+  if (T > 0 && (!lse || !zy)) return fail(DPPO_ERR_INVALID_ARG, "lse and zy are required");
+  const int es = esize_of(dtype);
+  if (dlogits_shard && T > 0) {
+    if (ld_dlogits < Vs)
+      return fail(DPPO_ERR_INVALID_ARG, "dlogits stride %lld < Vs = %lld", (long long)ld_dlogits, (long long)Vs);
+    const bool same = dlogits_shard == logits_shard && ld_dlogits == ld;
+    if (!same && overlaps(span_of(logits_shard, T, Vs, ld, es), span_of(dlogits_shard, T, Vs, ld_dlogits, es)))
+      return fail(DPPO_ERR_INVALID_ARG, "dlogits overlaps logits without aliasing them exactly");
+  }
+  hipStream_t st = (hipStream_t)stream;
+  dppo::launch_prep_stats(loss_mask, T, stats_out, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "prep_stats launch");
+  if (T > 0) {
+    dppo::ShardArgs a{};
+    dppo::RowArgs& r = a.a;
+    r.logits = logits_shard;
+    r.ld = ld;
+    r.dlogits = dlogits_shard;
+    r.ldd = ld_dlogits;
+    r.ids = token_ids;
+    r.lp_mu = logp_mu_old;
+    r.lp_ref = p->ref_mode == DPPO_REF_GIVEN ? logp_ref : nullptr;
+    r.ref_mode = p->ref_mode;
+    r.alpha = p->alpha;
+    r.adv = advantages;
+    r.mask = loss_mask;
+    r.tscale = token_scale;
+    r.lp_out = logp_out;
+    r.loss_tok = loss_tok_out;
+    r.flags = flags_out;
+    r.stats = stats_out;
+    r.T = (int32_t)T;
+    r.V = (int32_t)Vs;
+    r.mode = dppo::kModeLoss;
+    r.band_lo = p->band_lo;
+    r.band_hi = p->band_hi;
+    r.clip_lo = 1.0f - p->clip_eps_lo;
+    r.clip_hi = 1.0f + p->clip_eps_hi;
+    r.loss_scale = p->loss_scale;
+    r.rd_mode = p->rd_mode;
+    r.scale_mode = p->scale_mode;
+    a.vstart = vocab_start;
+    a.vtot = V;
+    a.lse_in = lse;
+    a.zy_in = zy;
+    const bool vec = aligned16(logits_shard) && (ld * es) % 16 == 0 &&
+                     (!dlogits_shard || (aligned16(dlogits_shard) && (ld_dlogits * es) % 16 == 0));
+    auto* ev = timer_slot();
+    if (ev) (void)hipEventRecord(ev->first, st);
+    e = dppo::launch_shard_loss(a, dtype == DPPO_BF16, vec, st);
+    if (ev) (void)hipEventRecord(ev->second, st);
+    if (e != hipSuccess) return hip_fail(e, "shard loss launch");
+  }
+  dppo::launch_loss_sum(loss_tok_out, loss_mask, token_scale, stats_out, T, p->loss_scale,
+                        p->scale_mode, loss_out, st);
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "loss_sum launch");
   return DPPO_OK;
 }
 

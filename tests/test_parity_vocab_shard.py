@@ -1,0 +1,199 @@
+"""GPU parity of the vocabulary-shard calls (through the C ABI) against the oracle's shard
+functions, and against the unsharded stage. The exchange between shards (an all-gather of
+the shard log-sum-exps, an all-reduce sum of z[y]) is done here with torch on one GPU: it is
+test glue standing in for the collectives, not part of the library."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_12070_amd as P
+from paper_2605_12070_amd import workloads as W
+
+from helpers import (TIGHT, assert_close_rel, bits_of, check_dlogits_rows, compare_loss,
+                     oracle_params, tie_mask, torch_anchor)
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _inputs(name, T, V, seed=None, mask_rows=(), bad_rows=()):
+    wl = W.make_workload(name, device=DEV, T=T, V=V, seed=seed, seq_len=min(32, T))
+    ids = wl.ids.clone()
+    for r in bad_rows:
+        ids[r] = wl.V + 7 if r % 2 else -3
+    mask = wl.mask.clone()
+    for r in mask_rows:
+        mask[r] = 0
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    return wl, ids, mask, lp_mu, lp_ref
+
+
+def _gpu_pipeline(logits, ids, mask, lp_mu, lp_ref, adv, cuts, kw, dlogits_full=None):
+    V = logits.shape[1]
+    stats = [P.vocab_shard_stats(logits[:, a:b], ids, a, V, mask) for a, b in zip(cuts, cuts[1:])]
+    lse = P.vocab_shard_combine(torch.stack([s[0] for s in stats]))    # all-gather stand-in
+    zy = torch.stack([s[1] for s in stats]).sum(dim=0)                 # all-reduce stand-in
+    outs = []
+    for a, b in zip(cuts, cuts[1:]):
+        d = None if dlogits_full is None else dlogits_full[:, a:b]
+        outs.append(P.decoupled_ppo_loss_shard_fwd_bwd(logits[:, a:b], a, V, lse, zy, ids, lp_mu,
+                                                       lp_ref, adv, mask, dlogits=d, **kw))
+    torch.cuda.synchronize()
+    return stats, lse, zy, outs
+
+
+@pytest.mark.parametrize("name,T,V,cuts", [
+    ("tiny", 256, 1024, (0, 1024)),
+    ("tiny", 256, 1024, (0, 1, 300, 512, 1024)),          # width-1 and unaligned shards
+    ("small_vocab", 384, 32000, (0, 4000, 8000, 12000, 16000, 20000, 24000, 28000, 32000)),
+    ("small_vocab", 384, 32000, (0, 10667, 21333, 32000)),  # uneven, unaligned
+])
+@pytest.mark.parametrize("rd_mode", ["mask_weight", "weight"])
+def test_shard_pipeline_matches_oracle(name, T, V, cuts, rd_mode):
+    _say("vocab shards", name, T, V, len(cuts) - 1, rd_mode)
+    wl, ids, mask, lp_mu, lp_ref = _inputs(name, T, V, mask_rows=(2, 40), bad_rows=(7, 8))
+    kw = dict(band=(0.5, 2.0), clip_eps=(0.1, 0.3), rd_mode=rd_mode, scale_mode="token_mean")
+    stats, lse, zy, outs = _gpu_pipeline(wl.logits, ids, mask, lp_mu, lp_ref, wl.adv, cuts, kw)
+    z = bits_of(wl.logits)
+    idn, mk = ids.cpu().numpy(), mask.cpu().numpy()
+    params = oracle_params((0.5, 2.0), (0.1, 0.3), rd_mode, "token_mean", 1.0)
+    rt = TIGHT
+    ref_stats = [oracle.vocab_shard_stats(z[:, a:b], idn, a, mk) for a, b in zip(cuts, cuts[1:])]
+    for (g_lse, g_zy), (r_lse, r_zy) in zip(stats, ref_stats):
+        gl = g_lse.cpu().double().numpy()
+        assert np.array_equal(np.isneginf(gl), np.isneginf(r_lse)), "-inf pattern of shard lse"
+        fin = np.isfinite(r_lse)
+        assert_close_rel(gl[fin], r_lse[fin], rt, "shard lse")
+        assert np.array_equal(g_zy.cpu().double().numpy(), r_zy), "shard z[y] (same bits)"
+    r_comb = oracle.vocab_shard_combine(np.stack([s[0] for s in ref_stats]))
+    assert_close_rel(lse.cpu().double().numpy(), r_comb, rt, "combined lse")
+    scale = oracle.batch_scale(mk, params)
+    for (a, b), out in zip(zip(cuts, cuts[1:]), outs):
+        ref = oracle.vocab_shard_loss(z[:, a:b], idn, a, V, lse.cpu().double().numpy(),
+                                      zy.cpu().double().numpy(), lp_mu.cpu().double().numpy(),
+                                      lp_ref.cpu().double().numpy(), wl.adv.cpu().double().numpy(),
+                                      mk, None, params, scale)
+        compare_loss(out, ref, params, wl.logits.dtype)
+        valid = ref["valid"]
+        ref_loss = float(np.sum(np.where(valid, ref["s"] * ref["loss_tok"], 0.0)))
+        bound = 1e-5 * float(np.sum(np.abs(np.where(valid, ref["s"] * ref["loss_tok"], 0.0)))) + 1e-12
+        assert abs(out.loss.item() - ref_loss) <= bound
+        ties = int(tie_mask(ref, params).sum())
+        got = out.stats.cpu().numpy().astype(np.int64)
+        want = oracle.stats_of(ref["flags"], params)
+        assert got[0] == want[0] and got[4] == want[4] and np.all(np.abs(got - want) <= ties)
+    # every shard reports the same per-token values
+    for out in outs[1:]:
+        assert torch.equal(out.logp.view(torch.int32), outs[0].logp.view(torch.int32))  # NaNs too
+        assert torch.equal(out.flags, outs[0].flags)
+    # and the sharded stage agrees with the unsharded call
+    full = P.decoupled_ppo_loss_fwd_bwd(wl.logits, ids, lp_mu, lp_ref, wl.adv, mask, **kw)
+    torch.cuda.synchronize()
+    assert_close_rel(outs[0].logp.cpu().double().numpy(), full.logp.cpu().double().numpy(),
+                     2e-5, "sharded vs unsharded lp")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_shard_dlogits_in_place_and_into_slices(dtype):
+    """dlogits written into column slices of one [T, V] tensor, and in place over the
+    logits, give the gradient of the unsharded call (up to the rounding of the output)."""
+    T, V, cuts = 200, 3000, (0, 700, 1500, 3000)
+    _say("vocab shards slices / in place", dtype)
+    g = torch.Generator(device=DEV).manual_seed(3)
+    logits = (torch.randn(T, V, generator=g, device=DEV) * 3).to(dtype)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    lp_ref = torch.randn(T, generator=g, device=DEV) * 0.2 - 8.0
+    lp_mu = lp_ref + torch.randn(T, generator=g, device=DEV) * 0.05
+    adv = torch.randn(T, generator=g, device=DEV)
+    kw = dict(scale_mode="const", loss_scale=1.0)
+    full = P.decoupled_ppo_loss_fwd_bwd(logits, ids, lp_mu, lp_ref, adv, None, **kw)
+    d_full = torch.empty_like(logits)
+    _gpu_pipeline(logits, ids, None, lp_mu, lp_ref, adv, cuts, kw, dlogits_full=d_full)
+    ref = oracle.decoupled_ppo_loss(bits_of(logits), ids.cpu().numpy(),
+                                    lp_mu.cpu().double().numpy(), lp_ref.cpu().double().numpy(),
+                                    adv.cpu().double().numpy(), None, None,
+                                    params=oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight",
+                                                         "const", 1.0))
+    ties = tie_mask(ref, oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0))
+    rows = np.nonzero(~ties)[0]
+    check_dlogits_rows(bits_of(d_full)[rows], ref["dlogits"][rows], ref["w"][rows], dtype)
+    # in place: every shard overwrites its own columns of the logits
+    z = logits.clone()
+    stats = [P.vocab_shard_stats(z[:, a:b], ids, a, V) for a, b in zip(cuts, cuts[1:])]
+    lse = P.vocab_shard_combine(torch.stack([s[0] for s in stats]))
+    zy = torch.stack([s[1] for s in stats]).sum(dim=0)
+    for a, b in zip(cuts, cuts[1:]):
+        v = z[:, a:b]
+        P.decoupled_ppo_loss_shard_fwd_bwd(v, a, V, lse, zy, ids, lp_mu, lp_ref, adv, dlogits=v, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(z, d_full), "in-place shard gradient differs from the out-of-place one"
+    del full
+
+
+def test_shard_all_neg_inf_row_and_empty_batch():
+    T, V = 8, 256
+    _say("vocab shards -inf row, empty")
+    logits = torch.randn(T, V, device=DEV)
+    logits[3] = float("-inf")
+    logits[4, :128] = float("-inf")                  # first shard of row 4 is all -inf
+    ids = torch.arange(T, device=DEV, dtype=torch.int64) * 20
+    s0 = P.vocab_shard_stats(logits[:, :128], ids, 0, V)
+    s1 = P.vocab_shard_stats(logits[:, 128:], ids, 128, V)
+    lse = P.vocab_shard_combine(torch.stack([s0[0], s1[0]]))
+    torch.cuda.synchronize()
+    assert s0[0][3].item() == float("-inf") and s0[0][4].item() == float("-inf")
+    assert np.isnan(lse[3].item())
+    ref = oracle.row_logsumexp(bits_of(logits[4:5, 128:]))[0]
+    assert abs(lse[4].item() - ref) <= 2e-5 * max(1.0, abs(ref))
+    e = torch.zeros(0, V, device=DEV)
+    z0 = torch.zeros(0, device=DEV)
+    l, zz = P.vocab_shard_stats(e[:, :10], torch.zeros(0, dtype=torch.int64, device=DEV), 0, V)
+    assert l.numel() == 0 and zz.numel() == 0
+    out = P.decoupled_ppo_loss_shard_fwd_bwd(e[:, :10], 0, V, z0, z0,
+                                             torch.zeros(0, dtype=torch.int64, device=DEV),
+                                             z0, z0, z0)
+    torch.cuda.synchronize()
+    assert out.loss.item() == 0.0 and out.stats.sum().item() == 0
+
+
+@pytest.mark.slow
+def test_shard_pipeline_full_size():
+    """large_vocab (T = 16384, V = 151936) over 8 shards of 18992 columns, the shape one GPU
+    of an 8-way vocabulary-parallel head holds: sampled rows against the oracle, and on every
+    row the gradient summed over all shards is zero."""
+    _say("vocab shards full size")
+    wl = W.make_workload("large_vocab", device=DEV)
+    T, V = wl.T, wl.V
+    lp_ref, lp_mu = W.reference_logprobs(torch_anchor(wl.logits, wl.ids), wl)
+    cuts = tuple(range(0, V + 1, V // 8))
+    assert cuts[-1] == V
+    d_full = torch.empty_like(wl.logits)
+    kw = dict(scale_mode="const", loss_scale=1.0)
+    _, lse, zy, outs = _gpu_pipeline(wl.logits, wl.ids, wl.mask, lp_mu, lp_ref, wl.adv, cuts, kw,
+                                     dlogits_full=d_full)
+    rows = np.sort(np.random.default_rng(5).choice(T, size=16, replace=False))
+    ridx = torch.as_tensor(rows, device=DEV)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    ref = oracle.decoupled_ppo_loss(bits_of(wl.logits[ridx]), wl.ids.cpu().numpy()[rows],
+                                    lp_mu.cpu().double().numpy()[rows],
+                                    lp_ref.cpu().double().numpy()[rows],
+                                    wl.adv.cpu().double().numpy()[rows], wl.mask.cpu().numpy()[rows],
+                                    None, params=params)
+    for out in outs:
+        compare_loss(out, ref, params, wl.logits.dtype, check_dlogits=False, rows=rows)
+    ties = tie_mask(ref, params)
+    ok = np.nonzero(~ties)[0]
+    check_dlogits_rows(bits_of(d_full[ridx])[ok], ref["dlogits"][ok], ref["w"][ok], torch.bfloat16)
+    # every row: the exact gradient sums to zero over the vocabulary, so the stored bf16 one
+    # sums to at most one rounding (2^-8 relative) of its magnitudes plus float32 error
+    for a in range(0, T, 2048):
+        d = d_full[a:a + 2048].float()
+        s, mag = d.sum(dim=1).abs(), d.abs().sum(dim=1)
+        assert bool((s <= (2.0 ** -8 + 1e-5) * mag + 1e-7).all()), f"row sums, rows {a}.."
+    del d_full
