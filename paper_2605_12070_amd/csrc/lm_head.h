@@ -9,11 +9,11 @@
 
 namespace dppo {
 
-// Tile of the GEMM kernels: LMH_WM x LMH_WN waves, each with LMH_TM x LMH_TN matrix-core
-// tiles of 32 x 32, so a workgroup of LMH_THREADS threads covers LMH_BM tokens x LMH_BN
-// vocabulary rows; K advances LMH_BK hidden features per LDS stage.
-constexpr int LMH_WM = 2, LMH_WN = 4;
-constexpr int LMH_TM = 4, LMH_TN = 2;
+// Tile of the GEMM kernels: LMH_WM x LMH_WN waves (one per SIMD), each with LMH_TM x LMH_TN
+// matrix-core tiles of 32 x 32, so a workgroup of LMH_THREADS threads covers LMH_BM tokens x
+// LMH_BN vocabulary rows; K advances LMH_BK hidden features per LDS stage.
+constexpr int LMH_WM = 2, LMH_WN = 2;
+constexpr int LMH_TM = 4, LMH_TN = 4;
 constexpr int LMH_BM = 32 * LMH_WM * LMH_TM;
 constexpr int LMH_BN = 32 * LMH_WN * LMH_TN;
 constexpr int LMH_BK = 64;

@@ -7,6 +7,9 @@
 //                  (ratios, band, PPO clip, loss, MIS weight w_t);
 //   lmh_bwd_tiles  recomputes a tile and writes g = w_t (softmax - onehot) for one
 //                  vocabulary chunk, the operand of the two gradient products.
+#include <type_traits>
+#include <utility>
+
 #include "dppo.h"
 #include "dppo_device.h"
 #include "lm_head.h"
@@ -23,16 +26,29 @@ namespace {
 // buffer-to-LDS loads (gfx950 writes lane l's 16 bytes at the wave's LDS base + 16 l, and
 // zeros for a lane whose offset lies outside the resource, which bounds every access to
 // the tile's rows and turns a K tail past d into zeros). There is no register staging:
-// LMH_STAGES LDS stages form a ring, and the loads of stage k + LMH_STAGES - 1 are issued
-// while stage k is multiplied. A stage holds the A and B tiles as rows of LMH_BK bf16 of K
-// (64 or 128 bytes); the 16-byte chunk c of row r sits at position c ^ sw(r), with
-// sw(r) = (r / 2) % 8 for 128-byte rows and (r / 4) % 4 for 64-byte rows, so the fragment
-// reads of 16 lanes (16 consecutive rows, one chunk) cover all 64 banks. Each stage is its
-// own LDS object, which lets the compiler track the loads into each separately.
+// LMH_STAGES LDS stages form a ring. A stage holds the A and B tiles as rows of LMH_BK bf16
+// of K (128 bytes); the 16-byte chunk c of row r sits at position c ^ sw(r), sw(r) = (r / 2)
+// % 8, so the fragment reads of 16 lanes (16 consecutive rows, one chunk) cover all 64 banks.
+// Each stage is its own LDS object, which lets the compiler track the loads into each
+// separately.
 // Wave (wm, wn) owns TM x TN tiles of 32 x 32 (v_mfma_f32_32x32x16_bf16, fp32 accumulation;
-// operand lane l holds row l % 32, K 8 (l / 32) .. +7). The vocabulary tile is the A operand,
-// so an accumulator holds vocabulary rows in its registers and tokens across its lanes: a
-// lane reduces over the vocabulary of its own tokens without crossing lanes (LmhLane below).
+// operand lane l holds row l % 32, K 8 (l / 32) .. +7). With 4 waves, one per SIMD, a wave
+// holds 128 x 128 accumulators in its 256 accumulation registers, which halves the LDS
+// fragment reads per matrix-core instruction against a 128 x 64 wave tile. The vocabulary
+// tile is the A operand, so an accumulator holds vocabulary rows in its registers and
+// tokens across its lanes: a lane reduces over the vocabulary of its own tokens without
+// crossing lanes (LmhLane below).
+// With a single wave per SIMD no other wave covers a stall, so the instruction order is
+// fixed by hand (scheduling fences between steps):
+//  * a K step of 16 is TM TN MFMAs; the fragments of the next K step are read during it,
+//    one read after each of the first TM + TN MFMAs (two fragment register sets, by the
+//    parity of the step);
+//  * the stage barrier sits before the last K step of a stage: by then every wave has read
+//    all of that stage's fragments, so its slot is refilled (with stage kb + LMH_STAGES)
+//    by loads spread one per MFMA over that last step, whose MFMAs also overlap the reads of
+//    the next stage's first fragments;
+//  * K is padded to whole turns of the ring; stages past d load zeros (the out-of-range
+//    offset) and add nothing, which keeps the loop free of branches.
 // After the K loop, epi(acc, scratch) runs on the accumulators, with the ring as scratch.
 constexpr int kWaves = LMH_WM * LMH_WN;
 constexpr int kChunks = LMH_BK / 8;             // 16-byte chunks per staged row
@@ -41,22 +57,26 @@ constexpr int kIA = LMH_BM / kRL / kWaves;      // loads per wave and stage, A
 constexpr int kIB = LMH_BN / kRL / kWaves;      // and B
 constexpr int kAEl = LMH_BM * LMH_BK;           // bf16 elements of the A tile (B follows)
 constexpr int kStageEl = (LMH_BM + LMH_BN) * LMH_BK;
-static_assert((LMH_BK == 64 || LMH_BK == 32) && LMH_BM % (kRL * kWaves) == 0 &&
-                  LMH_BN % (kRL * kWaves) == 0,
+static_assert(LMH_BK == 64 && LMH_BM % (kRL * kWaves) == 0 && LMH_BN % (kRL * kWaves) == 0,
               "tile shape");
 static_assert(LMH_WM * LMH_TM * LMH_WN * 32 * 8 <= LMH_STAGES * kStageEl * 2,
               "the forward merge scratch fits in the ring");
 static_assert(LMH_STAGES >= 2 && (LMH_STAGES - 2) * (kIA + kIB) <= 63, "ring depth");
+static_assert((LMH_BK / 16) % 2 == 0, "an even number of K steps per stage");
 
 // Swizzled position of 16-byte chunk c in staged row r.
-__device__ __forceinline__ int lmh_sw(int r) {
-  return LMH_BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
-}
+__device__ __forceinline__ int lmh_sw(int r) { return (r >> 1) & 7; }
+
+template <int N> using IC = std::integral_constant<int, N>;
 
 template <typename Epi>
 __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
                                            uint16_t* (&st)[LMH_STAGES], Epi&& epi) {
-  constexpr int TM = LMH_TM, TN = LMH_TN, BK = LMH_BK;
+  constexpr int TM = LMH_TM, TN = LMH_TN, BK = LMH_BK, KS = BK / 16, S = LMH_STAGES;
+  constexpr int L = kIA + kIB;                  // loads per wave and stage
+  constexpr int NF = TM + TN;                   // fragment reads per K step
+  constexpr int NM = TM * TN;                   // MFMAs per K step
+  constexpr int LPM = (L + NM - 1) / NM;        // refill loads per MFMA
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -80,23 +100,23 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
     const int row = kRL * (wave * kIB + i) + lane / kChunks;
     gob[i] = (row * d + ((lane % kChunks) ^ lmh_sw(row)) * 8) * 2;
   }
-  auto issue = [&](uint16_t* s, int kb) {
+  // refill load i of stage kb into slot s: i < kIA of the A tile, else of the B tile
+  auto load_one = [&](uint16_t* s, int kb, auto I) {
+    constexpr int i = decltype(I)::value;
     const int k0 = kb * BK;
-#pragma unroll
-    for (int i = 0; i < kIA; ++i) {
+    if constexpr (i < kIA) {
       const int row = kRL * (wave * kIA + i) + lane / kChunks;
       const int kc = (lane % kChunks) ^ lmh_sw(row);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           ra, (__attribute__((address_space(3))) void*)(s + (wave * kIA + i) * 512), 16,
           (k0 + kc * 8 < d) ? goa[i] + k0 * 2 : 0x7fffff00, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < kIB; ++i) {
-      const int row = kRL * (wave * kIB + i) + lane / kChunks;
+    } else {
+      constexpr int ib = i - kIA;
+      const int row = kRL * (wave * kIB + ib) + lane / kChunks;
       const int kc = (lane % kChunks) ^ lmh_sw(row);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rb, (__attribute__((address_space(3))) void*)(s + kAEl + (wave * kIB + i) * 512), 16,
-          (k0 + kc * 8 < d) ? gob[i] + k0 * 2 : 0x7fffff00, 0, 0, 0);
+          rb, (__attribute__((address_space(3))) void*)(s + kAEl + (wave * kIB + ib) * 512), 16,
+          (k0 + kc * 8 < d) ? gob[ib] + k0 * 2 : 0x7fffff00, 0, 0, 0);
     }
   };
 
@@ -108,41 +128,48 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
 
-  // Fragment reads run one K step ahead of the matrix-core instructions that use them.
-  auto frags = [&](const uint16_t* s, int ks, bf16x8 (&af)[TM], bf16x8 (&bfr)[TN]) {
-    const int kc = 2 * ks + (lane >> 5);
-#pragma unroll
-    for (int mi = 0; mi < TM; ++mi) {
-      const int R = wm * 32 * TM + mi * 32 + (lane & 31);
-      af[mi] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + R * BK + ((kc ^ lmh_sw(R)) * 8)));
-    }
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-      const int R = wn * 32 * TN + ni * 32 + (lane & 31);
-      bfr[ni] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + kAEl + R * BK + ((kc ^ lmh_sw(R)) * 8)));
-    }
+  // Fragment sets by K-step parity. A fragment row's swizzle depends only on lane % 32 (the
+  // rows of a wave's tiles step by 32), so every read is a per-lane base plus a constant.
+  bf16x8 fa[2][TM], fb[2][TN];
+  const int swz = lmh_sw(lane & 31);
+  const int rowa = (wm * 32 * TM + (lane & 31)) * BK;
+  const int rowb = kAEl + (wn * 32 * TN + (lane & 31)) * BK;
+  // fragment read i of K step ks of slot s into set f: i < TM the A fragment mi = i, else
+  // the B fragment ni = i - TM
+  auto read_one = [&](const uint16_t* s, int ks, auto F, auto I) {
+    constexpr int f = decltype(F)::value, i = decltype(I)::value;
+    const int col = ((2 * ks + (lane >> 5)) ^ swz) * 8;
+    if constexpr (i < TM)
+      fa[f][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + rowa + col + i * 32 * BK));
+    else
+      fb[f][i - TM] = __builtin_bit_cast(bf16x8, *(const u32x4*)(s + rowb + col + (i - TM) * 32 * BK));
   };
-  auto compute = [&](const uint16_t* s) {
-    bf16x8 a0[TM], b0[TN], a1[TM], b1[TN];
-    frags(s, 0, a0, b0);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ks += 2) {
-      frags(s, ks + 1, a1, b1);
-      __builtin_amdgcn_sched_barrier(0);       // keep the reads ahead of the MFMAs
-#pragma unroll
-      for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < TN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0[ni], a0[mi], acc[mi][ni], 0, 0, 0);
+  // MFMA i of a K step on set f: mi = i / TN, ni = i % TN
+  auto mfma_one = [&](auto F, auto I) {
+    constexpr int f = decltype(F)::value, i = decltype(I)::value;
+    acc[i / TN][i % TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        fb[f][i % TN], fa[f][i / TN], acc[i / TN][i % TN], 0, 0, 0);
+  };
+  // One K step on set f, reading K step rks of slot rs into set f ^ 1; with LOADS, the
+  // refill of slot dst with stage kb as well. Order per MFMA: read, loads, MFMA.
+  auto kstep = [&](auto F, const uint16_t* rs, int rks, auto LOADS, uint16_t* dst, int kb) {
+    constexpr int f = decltype(F)::value;
+    constexpr bool loads = decltype(LOADS)::value;
+    auto one = [&](auto I) {
+      constexpr int i = decltype(I)::value;
+      if constexpr (i < NF) read_one(rs, rks, IC<f ^ 1>{}, IC<i>{});
+      if constexpr (loads) {
+        [&]<int... vs>(std::integer_sequence<int, vs...>) {
+          ((i * LPM + vs < L ? load_one(dst, kb, IC<(i * LPM + vs < L ? i * LPM + vs : 0)>{})
+                             : void()), ...);
+        }(std::make_integer_sequence<int, LPM>{});
+      }
+      mfma_one(IC<f>{}, IC<i>{});
       __builtin_amdgcn_sched_barrier(0);
-      if (ks + 2 < BK / 16) frags(s, ks + 2, a0, b0);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < TN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1[ni], a1[mi], acc[mi][ni], 0, 0, 0);
-    }
+    };
+    [&]<int... is>(std::integer_sequence<int, is...>) {
+      (one(IC<is>{}), ...);
+    }(std::make_integer_sequence<int, NM>{});
   };
   // Barrier without a memory fence (a fence would wait for the loads still in flight); the
   // empty asm statements keep the compiler from moving memory accesses across it.
@@ -152,28 +179,35 @@ __device__ __forceinline__ void lmh_engine(const LmhArgs& m, int m0, int r0,
     asm volatile("" ::: "memory");
   };
 
-  constexpr int S = LMH_STAGES;
   const int nk = (d + BK - 1) / BK;
 #pragma unroll
-  for (int s = 0; s < S - 1; ++s)
-    if (s < nk) issue(st[s], s);
+  for (int s = 0; s < S; ++s)
+    [&]<int... vs>(std::integer_sequence<int, vs...>) {
+      (load_one(st[s], s, IC<vs>{}), ...);
+    }(std::make_integer_sequence<int, L>{});
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 1) * L) : "memory");
+  barrier();
+  [&]<int... is>(std::integer_sequence<int, is...>) {
+    (read_one(st[0], 0, IC<0>{}, IC<is>{}), ...);
+  }(std::make_integer_sequence<int, NF>{});
+  // stage kb in slot J
+  auto stage = [&](auto J, int kb) {
+    constexpr int j = decltype(J)::value;
+    [&]<int... ks>(std::integer_sequence<int, ks...>) {
+      (kstep(IC<ks & 1>{}, st[j], ks + 1, std::false_type{}, st[j], kb), ...);
+    }(std::make_integer_sequence<int, KS - 1>{});
+    // This wave's reads of slot j are done, and its loads of stage kb + 1 are once at most
+    // the loads of the S - 2 later stages are outstanding; after the barrier, every wave's.
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 2) * L) : "memory");
+    barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    kstep(IC<(KS - 1) & 1>{}, st[(j + 1) % S], 0, std::true_type{}, st[j], kb + S);
+  };
   for (int kb0 = 0; kb0 < nk; kb0 += S) {
-#pragma unroll
-    for (int j = 0; j < S; ++j) {
-      const int kb = kb0 + j;
-      if (kb < nk) {
-        // This wave's loads of stage kb are complete once at most the loads of the S - 2
-        // later stages are outstanding; after the barrier, every wave's are.
-        if (kb + S - 2 < nk) {
-          asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 2) * (kIA + kIB)) : "memory");
-        } else {
-          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        }
-        barrier();
-        if (kb + S - 1 < nk) issue(st[(j + S - 1) % S], kb + S - 1);
-        compute(st[j]);
-      }
-    }
+    [&]<int... js>(std::integer_sequence<int, js...>) {
+      (stage(IC<js>{}, kb0 + js), ...);
+    }(std::make_integer_sequence<int, S>{});
   }
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
   barrier();
