@@ -40,27 +40,29 @@ def log(*a):
 
 
 KERNEL_SOURCES = ("dppo_device.h", "loss_stage.h", "token_math.h", "loss_stage.hip")
+SHARD_SOURCES = ("dppo_device.h", "loss_stage.h", "token_math.h", "vocab_shard.h",
+                 "vocab_shard.hip")
 
 
-def kernel_source_hash() -> str:
-    """Hash of the row kernel's device sources, comments and spacing aside: a stored
-    HBM-traffic figure is reported only while it still describes the kernel being timed."""
+def kernel_source_hash(names=KERNEL_SOURCES) -> str:
+    """Hash of a kernel's device sources, comments and spacing aside: a stored HBM-traffic
+    figure is reported only while it still describes the kernel being timed."""
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in names:
         with open(os.path.join(CSRC, name)) as f:
             code = re.sub(r"/\*.*?\*/|//[^\n]*", "", f.read(), flags=re.S)   # comments
         h.update(name.encode() + " ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(key):
+def recorded_traffic(key, names=KERNEL_SOURCES):
     """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary, or None when
-    the kernel source has changed since the counters were taken."""
+    the kernel's sources (names) have changed since the counters were taken."""
     try:
         tr = json.load(open(TRAFFIC_FILE)).get(key)
     except (OSError, ValueError):
         return None
-    if tr and tr.get("source_hash") == kernel_source_hash():
+    if tr and tr.get("source_hash") == kernel_source_hash(names):
         return tr["bytes_per_launch"]
     return None
 
@@ -242,11 +244,13 @@ def vocab_shard_measure(dev, wl, lp_mu, lp_ref, n_shards=8, reps=20):
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBPS, 4), "kernel": "dppo::shard_loss<true, true>",
             "kernel_ms": round(k_loss, 4), "alg_bytes_per_launch": b_loss,
+            "traffic": recorded_traffic("vocab_shard_loss", SHARD_SOURCES),
             "shard": f"T={T} x Vs={Vs} (V/{n_shards}) bf16, contiguous",
             "stats_kernel": {"kernel": "dppo::shard_stats<true, true>",
                              "kernel_ms": round(k_stats, 4), "alg_bytes_per_launch": b_stats,
                              "achieved": round(b_stats / (k_stats * 1e-3) / 1e9, 1),
-                             "frac": round(b_stats / (k_stats * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
+                             "frac": round(b_stats / (k_stats * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                             "traffic": recorded_traffic("vocab_shard_stats", SHARD_SOURCES)},
             "step_ms": round(c_stats + c_loss, 4),
             "tokens_per_s": round(T / ((c_stats + c_loss) * 1e-3), 1)}
 
