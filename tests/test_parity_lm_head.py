@@ -100,8 +100,14 @@ def _run(T, d, V, seed=0, mask_frac=0.2, rd_mode="mask_weight", scale_mode="toke
 
 @pytest.mark.parametrize("rd_mode", ["none", "mask", "weight", "mask_weight"])
 def test_small_ragged(rd_mode):
-    # T and V not multiples of the 128 x 128 tile; d not a multiple of the 64-wide K step
+    # T and V not multiples of the 256 x 256 tile; d not a multiple of the 64-wide K step
     _run(200, 200, 1000, seed=1, rd_mode=rd_mode, bad_ids=(3, 4))
+
+
+def test_several_token_tiles_odd_stage_count():
+    # three token tiles (the last ragged), three vocabulary tiles, and d = 320: five K stages,
+    # an odd count, so the two-stage ring runs one padded stage of zeros
+    _run(600, 320, 700, seed=7)
 
 
 def test_const_scale_and_unit_loss():
