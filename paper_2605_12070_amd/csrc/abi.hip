@@ -281,6 +281,8 @@ const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t w
   const char* bw = with_dlogits ? "true" : "false";
   if (L.resident && dtype == DPPO_BF16 && !with_dlogits)
     snprintf(buf, sizeof(buf), "dppo::rows_bf16_fwd<%d, %d>", L.threads, L.chunks);
+  else if (L.two_buffers)
+    snprintf(buf, sizeof(buf), "dppo::rows_bf16_resident_db<%d, %d>", L.threads, L.chunks);
   else if (L.resident)
     snprintf(buf, sizeof(buf), "dppo::rows_%s_resident<%d, %d, %s>", ty, L.threads, L.chunks, bw);
   else

@@ -64,6 +64,7 @@ struct RowLaunch {
   int chunks = 0;            // resident kernels: 16-byte chunks per thread
   bool resident = false;
   bool persistent = false;  // grid = resident workgroups on the device, rows looped over
+  bool two_buffers = false; // resident backward kernel with two row buffers
 };
 
 RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force);

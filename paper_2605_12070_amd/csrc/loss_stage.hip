@@ -49,7 +49,7 @@ __device__ __forceinline__ bool version_ok(const A& a, int64_t row) {
 
 // Rows that are not evaluated (loss mask 0, or a bad token id on a valid row).
 template <typename Tin, int NT>
-__device__ void skip_row(const RowArgs& a, int64_t row, bool valid) {
+__device__ void skip_row(const RowArgs& a, int64_t row, bool valid, StatCount& sc) {
   if (a.dlogits) {
     Tin* d = (Tin*)a.dlogits + row * a.ldd;
     for (int v = threadIdx.x; v < a.V; v += NT) d[v] = (Tin)0;
@@ -58,14 +58,14 @@ __device__ void skip_row(const RowArgs& a, int64_t row, bool valid) {
     a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
     a.loss_tok[row] = 0.0f;
     if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
-    if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+    if (valid) sc.bad += 1;
   }
 }
 
 // Zero dlogits row for the register-resident paths: NC 16-byte buffer stores per thread
 // (stores past the row are dropped by the buffer range check) plus a ragged tail.
 template <int NT, int NC, int ES>
-__device__ void skip_row_resident(const RowArgs& a, int64_t row, bool valid) {
+__device__ void skip_row_resident(const RowArgs& a, int64_t row, bool valid, StatCount& sc) {
   if (a.dlogits) {
     constexpr int E = 16 / ES;
     char* d = (char*)a.dlogits + row * a.ldd * ES;
@@ -84,7 +84,7 @@ __device__ void skip_row_resident(const RowArgs& a, int64_t row, bool valid) {
     a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
     a.loss_tok[row] = 0.0f;
     if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
-    if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+    if (valid) sc.bad += 1;
   }
 }
 
@@ -102,7 +102,8 @@ struct Bcast {
 };
 
 __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float zy,
-                                           float lse2, bool good, Bcast* bc, const TokenIn& tin) {
+                                           float lse2, bool good, Bcast* bc, const TokenIn& tin,
+                                           StatCount& sc) {
   if (a.mode == kModeLogprob) {
     if (threadIdx.x == 0) {
       a.lp_out[row] = good ? zy - lse2 * kLn2 : __builtin_nanf("");
@@ -115,7 +116,7 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
     a.lp_out[row] = o.lp;
     a.loss_tok[row] = o.loss;
     if (a.flags) a.flags[row] = o.flags;
-    count_stats(a, o.flags);
+    count_stats(a, o.flags, sc);
     bc->w = o.w;
     bc->lse2 = lse2;
     bc->dy = o.dy;
@@ -138,9 +139,14 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 //           flight while this row's stores drain. Stores go first because the vector
 //           memory counter retires in order: a load queued behind a store would make the
 //           next row's first wait also wait for that store.
+// With DB (two row buffers, for shapes whose registers allow it) the next row's loads go
+// out as soon as this row has arrived, into the other buffer, before this row's stores;
+// the next row's wait then leaves this row's NC stores outstanding (vmcnt(NC)). Rows of a
+// few tens of KiB otherwise run in lockstep across the chip: every workgroup loads, then
+// computes, then stores, and reads and writes never overlap.
 // ---------------------------------------------------------------------------------------
-template <int NT, int NC, bool BWD>
-__global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
+template <int NT, int NC, bool BWD, bool DB>
+__device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   __shared__ float red[2][2 * (NT / 64)];   // alternated by row parity: one barrier per merge
   __shared__ Bcast bc;
   // Per-chunk shifts n_c live in LDS (NC x NT floats, conflict-free [c][tid] layout): the
@@ -159,7 +165,9 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
   // Every load and store of the row goes through a buffer resource; a resource with
   // num_records = 0 turns an access into a no-op (loads read zeros, stores are dropped),
   // which keeps the chunk loops free of branches.
-  uint32_t r[NC][4];
+  uint32_t r1[NC][4];
+  uint32_t r2[DB ? NC : 1][4];             // the second row buffer (DB)
+  StatCount sc;                            // thread 0's counters over this workgroup's rows
   int64_t row = blockIdx.x;
   // Stagger the start of the workgroups that share an XCD: workgroups are dealt to the
   // eight XCDs in turn, so blockIdx / 8 numbers them within their XCD. Started together,
@@ -175,14 +183,21 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
     const __amdgpu_buffer_rsrc_t rz =
         row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
 #pragma unroll
-    for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
+    for (int c = 0; c < NC; ++c) load16(r1[c], rz, threadIdx.x * 16, c * NT * 16);
   }
   int parity = 0;
-  for (; row < a.T; row += gridDim.x, parity ^= 1) {
-    // Start a row only once all of it has arrived (and the previous row's stores have
-    // drained), rather than consuming chunks as they land: measured faster on MI355X,
-    // by 1-2 %, with the staggered starts and the reduced grid described above.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // One row: its chunks are in r (cur); nx receives the next row's chunks (nx is r itself
+  // without DB). `first`: nothing but this row's loads is outstanding.
+  auto step = [&](uint32_t (&r)[NC][4], uint32_t (&nx)[NC][4], bool first) {
+    // Start a row only once all of it has arrived, rather than consuming chunks as they
+    // land: measured faster on MI355X, by 1-2 %, with the staggered starts and the reduced
+    // grid described above. Without DB this also waits for the previous row's stores; with
+    // DB at least NC stores of the previous row were issued after this row's loads.
+    if (DB && want_d && !first) {
+      asm volatile("s_waitcnt vmcnt(%0)" :: "n"(NC) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
     const int tid = threadIdx.x;
     const int V = a.V;
     const int voff = tid * 16;
@@ -195,6 +210,12 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
 
     const int64_t next = row + gridDim.x;
     const bool rd_next = next < a.T && reads(next);
+    const __amdgpu_buffer_rsrc_t rn = row_rsrc(
+        row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
+    if constexpr (DB) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) load16(nx[c], rn, voff, c * NT * 16);
+    }
     const int64_t y = uload(a.ids + row);
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
     const TokenIn tin = token_inputs(a, row);   // scalar loads, in flight during pass A
@@ -250,7 +271,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
       block_merge_ns_int<NT>(n, s, red[parity]);
       // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
       const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
-      finish_row(a, row, zy, lse2, good, &bc, tin);
+      finish_row(a, row, zy, lse2, good, &bc, tin, sc);
       if (want_d) {
         __syncthreads();
         w = bc.w;
@@ -270,7 +291,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
       a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
       a.loss_tok[row] = 0.0f;
       if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
-      if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+      if (valid) sc.bad += 1;
     }
 
     // Pass B: dlogits of this row, then the only place the registers are refilled: the
@@ -278,8 +299,6 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
     // zeros are written below.
     uint16_t* drow = want_d ? (uint16_t*)a.dlogits + row * a.ldd : nullptr;
     const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, (want_d && rd_cur) ? V * 2 : 0);
-    const __amdgpu_buffer_rsrc_t rn = row_rsrc(
-        row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
     const float wf = rd_cur ? w : 0.0f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -307,8 +326,10 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
     // All of this row's stores are issued before any load of the next row: the vector
     // memory counter retires in order, and loads queued behind interleaved stores would
     // make every wait in the next row's pass A also wait for store acknowledgements.
+    if constexpr (!DB) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) load16(r[c], rn, voff, c * NT * 16);
+      for (int c = 0; c < NC; ++c) load16(nx[c], rn, voff, c * NT * 16);
+    }
     if (want_d && !rd_cur) {                // zeros for a row that was not read
       const __amdgpu_buffer_rsrc_t rz = row_rsrc(drow, V * 2);
       const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -321,7 +342,35 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
     if (want_d && rd_cur && good && tid == (int)((y >> 3) % NT))
       __builtin_amdgcn_raw_buffer_store_b16(to_bf16(dy), rd, (int)(y * 2), 0, kAuxNT);
     rd_cur = rd_next;
+  };
+  if constexpr (DB) {
+    // unrolled twice, so that the buffers swap roles without register copies
+    bool first = true;
+    while (row < a.T) {
+      step(r1, r2, first);
+      first = false;
+      row += gridDim.x;
+      parity ^= 1;
+      if (row >= a.T) break;
+      step(r2, r1, false);
+      row += gridDim.x;
+      parity ^= 1;
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the loads past the last row
+  } else {
+    for (; row < a.T; row += gridDim.x, parity ^= 1) step(r1, r1, false);
   }
+  if (threadIdx.x == 0) flush_stats(a, sc);
+}
+
+template <int NT, int NC, bool BWD>
+__global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
+  resident_rows<NT, NC, BWD, false>(a);
+}
+// The two-buffer form, with dlogits (the backward kernel).
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_bf16_resident_db(RowArgs a) {
+  resident_rows<NT, NC, true, true>(a);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -345,6 +394,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
     return yy >= 0 && yy < a.V;
   };
   uint32_t r[NC][4];
+  StatCount sc;
   int64_t row = blockIdx.x;
   if (a.T >= 4 * (int64_t)gridDim.x) {      // staggered starts, as in rows_bf16_resident
     const int steps = (int)((blockIdx.x >> 3) & 31);
@@ -408,16 +458,17 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
     if (rd_cur) {
       block_merge_ns_int<NT>(N, S, red[parity]);
       const float lse2 = (N == -INFINITY) ? __builtin_nanf("") : N + log2f(S);
-      finish_row(a, row, zy, lse2, good, &bc, tin);
+      finish_row(a, row, zy, lse2, good, &bc, tin, sc);
     } else if (tid == 0) {                  // masked row, or a bad id on a valid loss row
       const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
       a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
       a.loss_tok[row] = 0.0f;
       if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
-      if (valid) atomicAdd(&a.stats[DPPO_STAT_N_BAD], 1);
+      if (valid) sc.bad += 1;
     }
     rd_cur = rd_next;
   }
+  if (threadIdx.x == 0) flush_stats(a, sc);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -427,111 +478,116 @@ template <int NT, int NC, bool BWD>
 __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
-  const int64_t row = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int V = a.V;
-  const int nfull = V >> 2;
-  const bool loss_mode = a.mode != kModeLogprob;
-  const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
-  const int64_t y = a.ids[row];
-  const bool good = (y >= 0) && (y < V) && version_ok(a, row);
-  if (loss_mode && !(valid && good)) {
-    skip_row_resident<NT, NC, 4>(a, row, valid);
-    return;
-  }
-  const float* zrow = row_ptr<float>(a, row);
-  float zy = 0.0f;
-  if (tid == 0 && good) zy = zrow[y];
-
-  const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, V * 4);
-  const int voff = tid * 16;
-  float r[NC][4];
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const u32x4 v = buf_load16(rz, voff, c * NT * 16);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) r[c][j] = __uint_as_float(v[j]);
-  }
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    if ((c + 1) * NT > nfull && c * NT + tid >= nfull) {
-      r[c][0] = r[c][1] = r[c][2] = r[c][3] = -INFINITY;
+  StatCount sc;
+  // one row; the merge's second barrier orders the LDS reuse between consecutive rows
+  auto one = [&](const int64_t row) {
+    const int tid = threadIdx.x;
+    const int V = a.V;
+    const int nfull = V >> 2;
+    const bool loss_mode = a.mode != kModeLogprob;
+    const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
+    const int64_t y = a.ids[row];
+    const bool good = (y >= 0) && (y < V) && version_ok(a, row);
+    if (loss_mode && !(valid && good)) {
+      skip_row_resident<NT, NC, 4>(a, row, valid, sc);
+      return;
     }
-  }
-  const int tail_slot = nfull / NT;
-  const bool tail_owner = (V & 3) != 0 && tid == nfull % NT;
-  if (tail_owner) {
+    const float* zrow = row_ptr<float>(a, row);
+    float zy = 0.0f;
+    if (tid == 0 && good) zy = zrow[y];
+
+    const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, V * 4);
+    const int voff = tid * 16;
+    float r[NC][4];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      if (c == tail_slot) {
+      const u32x4 v = buf_load16(rz, voff, c * NT * 16);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int e = nfull * 4 + j;
-          if (e < V) r[c][j] = zrow[e];
+      for (int j = 0; j < 4; ++j) r[c][j] = __uint_as_float(v[j]);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if ((c + 1) * NT > nfull && c * NT + tid >= nfull) {
+        r[c][0] = r[c][1] = r[c][2] = r[c][3] = -INFINITY;
+      }
+    }
+    const int tail_slot = nfull / NT;
+    const bool tail_owner = (V & 3) != 0 && tid == nfull % NT;
+    if (tail_owner) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        if (c == tail_slot) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int e = nfull * 4 + j;
+            if (e < V) r[c][j] = zrow[e];
+          }
         }
       }
     }
-  }
 
-  float m = -INFINITY;
+    float m = -INFINITY;
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    m = max3(m, r[c][0], r[c][1]);
-    m = max3(m, r[c][2], r[c][3]);
-  }
-  const float n_shift = (m == -INFINITY) ? 0.0f : m * kLog2e;
-  const float nb = -n_shift;
-  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    float e[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) e[j] = exp2_hw(__builtin_fmaf(r[c][j], kLog2e, nb));
-    s0 += e[0]; s1 += e[1]; s2 += e[2]; s3 += e[3];
-    if (BWD) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) r[c][j] = e[j];
+    for (int c = 0; c < NC; ++c) {
+      m = max3(m, r[c][0], r[c][1]);
+      m = max3(m, r[c][2], r[c][3]);
     }
-  }
-  float n = (m == -INFINITY) ? -INFINITY : n_shift;
-  float s = (s0 + s1) + (s2 + s3);
-  const float n_mine = n;
-  block_merge_ns<NT>(n, s, red);
-  const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
-
-  finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row));
-  if (!BWD || !a.dlogits) return;
-  __syncthreads();
-  const float w = bc.w;
-  const float dy = bc.dy;
-  const float f = row_factor(w, n_mine, bc.lse2);
-  float* drow = (float*)a.dlogits + row * a.ldd;
-  const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, V * 4);
-  const int cy = (int)(y >> 2);
-  const int my_slot = (cy % NT == tid) ? cy / NT : -1;
-  const int jy = (int)(y & 3);
+    const float n_shift = (m == -INFINITY) ? 0.0f : m * kLog2e;
+    const float nb = -n_shift;
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int idx = c * NT + tid;
-    float o[4];
+    for (int c = 0; c < NC; ++c) {
+      float e[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = r[c][j] * f;
-    if (c == my_slot) {
+      for (int j = 0; j < 4; ++j) e[j] = exp2_hw(__builtin_fmaf(r[c][j], kLog2e, nb));
+      s0 += e[0]; s1 += e[1]; s2 += e[2]; s3 += e[3];
+      if (BWD) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) o[j] = (j == jy) ? dy : o[j];
-    }
-    if ((c + 1) * NT <= nfull || idx < nfull) {
-      const u32x4 v = {__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
-                       __float_as_uint(o[3])};
-      buf_store16_nt(v, rd, voff, c * NT * 16);
-    } else if (tail_owner && c == tail_slot) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = nfull * 4 + j;
-        if (e < V) drow[e] = o[j];
+        for (int j = 0; j < 4; ++j) r[c][j] = e[j];
       }
     }
-  }
+    float n = (m == -INFINITY) ? -INFINITY : n_shift;
+    float s = (s0 + s1) + (s2 + s3);
+    const float n_mine = n;
+    block_merge_ns<NT>(n, s, red);
+    const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+
+    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    if (!BWD || !a.dlogits) return;
+    __syncthreads();
+    const float w = bc.w;
+    const float dy = bc.dy;
+    const float f = row_factor(w, n_mine, bc.lse2);
+    float* drow = (float*)a.dlogits + row * a.ldd;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, V * 4);
+    const int cy = (int)(y >> 2);
+    const int my_slot = (cy % NT == tid) ? cy / NT : -1;
+    const int jy = (int)(y & 3);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int idx = c * NT + tid;
+      float o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = r[c][j] * f;
+      if (c == my_slot) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = (j == jy) ? dy : o[j];
+      }
+      if ((c + 1) * NT <= nfull || idx < nfull) {
+        const u32x4 v = {__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                         __float_as_uint(o[3])};
+        buf_store16_nt(v, rd, voff, c * NT * 16);
+      } else if (tail_owner && c == tail_slot) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int e = nfull * 4 + j;
+          if (e < V) drow[e] = o[j];
+        }
+      }
+    }
+  };
+  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) one(row);
+  if (threadIdx.x == 0) flush_stats(a, sc);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -612,56 +668,61 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgsOf<BWD> a) {
   constexpr int E = C::E;
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
-  const int64_t row = blockIdx.x;
-  const int tid = threadIdx.x;
-  const int V = a.V;
-  const int nchunk = (V + E - 1) / E;
-  const bool loss_mode = a.mode != kModeLogprob;
-  const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
-  const int64_t y = a.ids[row];
-  const bool good = (y >= 0) && (y < V) && version_ok(a, row);
-  if (loss_mode && !(valid && good)) {
-    skip_row<Tin, NT>(a, row, valid);
-    return;
-  }
-  const Tin* zrow = row_ptr<Tin>(a, row);
-  float zy = 0.0f;
-  if (tid == 0 && good) zy = load_elem<Tin>(zrow, y);
-
-  float n = -INFINITY, s = 0.0f;
-  for (int idx = tid; idx < nchunk; idx += NT) {
-    float x[E];
-    C::load(zrow, idx, V, x);
-    float m = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < E; ++j) m = fmaxf(m, x[j]);
-    const float ns = (m == -INFINITY) ? 0.0f : m * kLog2e;
-    float cs = 0.0f;
-#pragma unroll
-    for (int j = 0; j < E; ++j) cs += exp2_hw(__builtin_fmaf(x[j], kLog2e, -ns));
-    merge_ns(n, s, (m == -INFINITY) ? -INFINITY : ns, cs);
-  }
-  block_merge_ns<NT>(n, s, red);
-  const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
-
-  finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row));
-  if (!BWD || !a.dlogits) return;
-  __syncthreads();
-  const float w = bc.w;
-  const float dy = bc.dy;
-  const float nl = -bc.lse2;
-  Tin* drow = (Tin*)a.dlogits + row * a.ldd;
-  for (int idx = tid; idx < nchunk; idx += NT) {
-    float x[E];
-    C::load(zrow, idx, V, x);
-    float o[E];
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-      o[j] = w * exp2_hw(__builtin_fmaf(x[j], kLog2e, nl));
-      if ((int64_t)idx * E + j == y) o[j] = dy;
+  StatCount sc;
+  // one row; the merge's second barrier orders the LDS reuse between consecutive rows
+  auto one = [&](const int64_t row) {
+    const int tid = threadIdx.x;
+    const int V = a.V;
+    const int nchunk = (V + E - 1) / E;
+    const bool loss_mode = a.mode != kModeLogprob;
+    const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
+    const int64_t y = a.ids[row];
+    const bool good = (y >= 0) && (y < V) && version_ok(a, row);
+    if (loss_mode && !(valid && good)) {
+      skip_row<Tin, NT>(a, row, valid, sc);
+      return;
     }
-    C::store(drow, idx, V, o);
-  }
+    const Tin* zrow = row_ptr<Tin>(a, row);
+    float zy = 0.0f;
+    if (tid == 0 && good) zy = load_elem<Tin>(zrow, y);
+
+    float n = -INFINITY, s = 0.0f;
+    for (int idx = tid; idx < nchunk; idx += NT) {
+      float x[E];
+      C::load(zrow, idx, V, x);
+      float m = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < E; ++j) m = fmaxf(m, x[j]);
+      const float ns = (m == -INFINITY) ? 0.0f : m * kLog2e;
+      float cs = 0.0f;
+#pragma unroll
+      for (int j = 0; j < E; ++j) cs += exp2_hw(__builtin_fmaf(x[j], kLog2e, -ns));
+      merge_ns(n, s, (m == -INFINITY) ? -INFINITY : ns, cs);
+    }
+    block_merge_ns<NT>(n, s, red);
+    const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+
+    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    if (!BWD || !a.dlogits) return;
+    __syncthreads();
+    const float w = bc.w;
+    const float dy = bc.dy;
+    const float nl = -bc.lse2;
+    Tin* drow = (Tin*)a.dlogits + row * a.ldd;
+    for (int idx = tid; idx < nchunk; idx += NT) {
+      float x[E];
+      C::load(zrow, idx, V, x);
+      float o[E];
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        o[j] = w * exp2_hw(__builtin_fmaf(x[j], kLog2e, nl));
+        if ((int64_t)idx * E + j == y) o[j] = dy;
+      }
+      C::store(drow, idx, V, o);
+    }
+  };
+  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) one(row);
+  if (threadIdx.x == 0) flush_stats(a, sc);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -744,6 +805,17 @@ struct ResCfg {
 constexpr ResCfg kResident[] = {{256, 1},  {256, 2},   {256, 4},   {512, 4},   {512, 6},
                                 {512, 8},  {1024, 6}, {1024, 8}, {1024, 12}, {1024, 19}};
 constexpr int kNumResident = sizeof(kResident) / sizeof(kResident[0]);
+// Per-shape launch choices, each from same-box A/B timings at T = 16384 (MI355X):
+//  * bf16 backward with two row buffers: 5-10 % faster for 512 x 4 .. 1024 x 8; within
+//    +-4 % (either way) for the 256-thread shapes and 1024 x 12; 1024 x 19 has no registers
+//    for a second row;
+//  * fp32 persistent (a loop over rows, counters flushed once per workgroup) rather than one
+//    workgroup per row: 2-6x faster up to 512 x 8 and 6 % at 1024 x 19, 0-7 % slower for
+//    1024 x 6 .. 1024 x 12.
+constexpr bool kResidentDB[kNumResident] = {false, false, false, true, true,
+                                            true,  true,  true,  false, false};
+constexpr bool kF32Persistent[kNumResident] = {true,  true,  true,  true,  true,
+                                               true,  false, false, false, true};
 
 const void* pick_bf16_fwd(int i) {
   switch (i) {
@@ -757,6 +829,17 @@ const void* pick_bf16_fwd(int i) {
     case 7: return (const void*)rows_bf16_fwd<1024, 8>;
     case 8: return (const void*)rows_bf16_fwd<1024, 12>;
     default: return (const void*)rows_bf16_fwd<1024, 19>;
+  }
+}
+// Two-buffer backward kernels, for the shapes kResidentDB selects.
+const void* pick_bf16_db(int i) {
+  switch (i) {
+    case 3: return (const void*)rows_bf16_resident_db<512, 4>;
+    case 4: return (const void*)rows_bf16_resident_db<512, 6>;
+    case 5: return (const void*)rows_bf16_resident_db<512, 8>;
+    case 6: return (const void*)rows_bf16_resident_db<1024, 6>;
+    case 7: return (const void*)rows_bf16_resident_db<1024, 8>;
+    default: return nullptr;
   }
 }
 template <bool BWD>
@@ -809,10 +892,13 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   if (pick >= 0) {
     L.threads = kResident[pick].nt;
     L.chunks = kResident[pick].nc;
-    L.fn = dtype == DPPO_BF16 ? (bwd ? pick_bf16<true>(pick) : pick_bf16_fwd(pick))
-                              : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
+    L.fn = dtype == DPPO_BF16
+               ? (bwd ? (kResidentDB[pick] ? pick_bf16_db(pick) : pick_bf16<true>(pick))
+                      : pick_bf16_fwd(pick))
+               : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
+    L.two_buffers = dtype == DPPO_BF16 && bwd && kResidentDB[pick];
     L.resident = true;
-    L.persistent = dtype == DPPO_BF16;
+    L.persistent = dtype == DPPO_BF16 || kF32Persistent[pick];
     return L;
   }
   L.threads = 1024;

@@ -97,13 +97,27 @@ __device__ __forceinline__ float row_scale(const RowArgs& a) {
   return a.loss_scale;
 }
 
-__device__ __forceinline__ void count_stats(const RowArgs& a, uint8_t flags) {
+// A workgroup's counters, kept by thread 0 over all of its rows and added to the global
+// counters once, when the workgroup ends: device-scope atomics on the same five addresses
+// serialise, and one per row made a batch of short rows wait on them.
+struct StatCount {
+  int band = 0, ppo = 0, active = 0, bad = 0;
+};
+
+__device__ __forceinline__ void count_stats(const RowArgs& a, uint8_t flags, StatCount& sc) {
   const bool band = flags & DPPO_FLAG_BAND;
   const bool ppo = flags & DPPO_FLAG_PPO;
   const bool uses_mask = a.rd_mode == DPPO_RD_MASK || a.rd_mode == DPPO_RD_MASK_WEIGHT;
-  if (band) atomicAdd(&a.stats[DPPO_STAT_N_BAND], 1);
-  if (ppo) atomicAdd(&a.stats[DPPO_STAT_N_PPO], 1);
-  if (ppo && (band || !uses_mask)) atomicAdd(&a.stats[DPPO_STAT_N_ACTIVE], 1);
+  sc.band += band;
+  sc.ppo += ppo;
+  sc.active += ppo && (band || !uses_mask);
+}
+
+__device__ __forceinline__ void flush_stats(const RowArgs& a, const StatCount& sc) {
+  if (sc.band) atomicAdd(&a.stats[DPPO_STAT_N_BAND], sc.band);
+  if (sc.ppo) atomicAdd(&a.stats[DPPO_STAT_N_PPO], sc.ppo);
+  if (sc.active) atomicAdd(&a.stats[DPPO_STAT_N_ACTIVE], sc.active);
+  if (sc.bad) atomicAdd(&a.stats[DPPO_STAT_N_BAD], sc.bad);
 }
 
 

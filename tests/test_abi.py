@@ -234,6 +234,12 @@ def test_row_kernel_name_follows_the_selection_rule():
     assert row_kernel_name(bf, 77825).startswith("dppo::rows_stream")      # ragged chunk
     assert row_kernel_name(bf, 64, ld=68).endswith("true, false>")          # unaligned stride
     assert row_kernel_name(f32, 32000) == "dppo::rows_f32_resident<1024, 8, true>"
+    # two row buffers for the bf16 backward shapes 512 x 4 .. 1024 x 8 only
+    assert row_kernel_name(bf, 32000) == "dppo::rows_bf16_resident_db<512, 8>"
+    assert row_kernel_name(bf, 65536) == "dppo::rows_bf16_resident_db<1024, 8>"
+    assert row_kernel_name(bf, 98000) == "dppo::rows_bf16_resident<1024, 12, true>"
+    assert row_kernel_name(bf, 8192) == "dppo::rows_bf16_resident<256, 4, true>"
+    assert row_kernel_name(bf, 32000, with_dlogits=False) == "dppo::rows_bf16_fwd<512, 8>"
     L = _lib.lib()
     assert L.dppo_row_kernel_name(7, 100, 100, 1) is None
     assert L.dppo_row_kernel_name(1, 0, 0, 1) is None

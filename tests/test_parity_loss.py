@@ -168,6 +168,58 @@ def test_ragged_vocab_sizes(dtype, V):
         compare_loss(res, ref, params, dtype)
 
 
+# One case per register-resident shape, with more rows than the grid has workgroups, so
+# that a workgroup loops over at least three rows: both row buffers of the two-buffer
+# kernels serve twice, and the persistent fp32 loop and the per-workgroup counters are
+# exercised. Every 7th row is masked and a few valid rows carry bad ids, so rows that are
+# not read (zero stores) alternate with rows that are.
+RESIDENT_CASES = [
+    (torch.bfloat16, 2000, 4600, "rows_bf16_resident<256, 1, true>"),
+    (torch.bfloat16, 4000, 4600, "rows_bf16_resident<256, 2, true>"),
+    (torch.bfloat16, 8192, 4600, "rows_bf16_resident<256, 4, true>"),
+    (torch.bfloat16, 16000, 2000, "rows_bf16_resident_db<512, 4>"),
+    (torch.bfloat16, 24000, 1400, "rows_bf16_resident_db<512, 6>"),
+    (torch.bfloat16, 32000, 1400, "rows_bf16_resident_db<512, 8>"),
+    (torch.bfloat16, 49000, 700, "rows_bf16_resident_db<1024, 6>"),
+    (torch.bfloat16, 65536, 700, "rows_bf16_resident_db<1024, 8>"),
+    (torch.bfloat16, 98000, 700, "rows_bf16_resident<1024, 12, true>"),
+    (torch.float32, 1000, 4600, "rows_f32_resident<256, 1, true>"),
+    (torch.float32, 4000, 4600, "rows_f32_resident<256, 4, true>"),
+    (torch.float32, 8000, 2000, "rows_f32_resident<512, 4, true>"),
+    (torch.float32, 16000, 1400, "rows_f32_resident<512, 8, true>"),
+    (torch.float32, 24000, 700, "rows_f32_resident<1024, 6, true>"),
+    (torch.float32, 76000, 700, "rows_f32_resident<1024, 19, true>"),
+]
+
+
+@pytest.mark.parametrize("dtype,V,T,kernel", RESIDENT_CASES,
+                         ids=[c[3].split("<")[0][5:] + f"_V{c[1]}" for c in RESIDENT_CASES])
+def test_every_resident_shape_several_rows_per_workgroup(dtype, V, T, kernel):
+    _say("resident shape", dtype, V, T, kernel)
+    assert P.row_kernel_name(dtype, V) == "dppo::" + kernel
+    g = torch.Generator(device=DEV).manual_seed(V + T)
+    z = (torch.randn(T, V, generator=g, device=DEV) * 3).to(dtype)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[5::97] = V + 1                                  # bad ids on valid rows
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    mask[::7] = 0
+    anchor = oracle_anchor(z, ids.clamp(0, V - 1)).to(DEV)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.3 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask)
+    torch.cuda.synchronize()
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    n_ties = compare_loss(res, ref, params, dtype)
+    fl = res.flags.cpu().numpy()
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
+    diff = np.abs(st.astype(np.int64) - np.asarray(ref["stats"], np.int64))
+    assert diff[0] == 0 and diff[4] == 0 and np.all(diff <= n_ties), (st, ref["stats"], n_ties)
+    assert st[4] == int(((ids.cpu().numpy() > V) & (mask.cpu().numpy() != 0)).sum()) > 0
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_unaligned_and_strided_rows(dtype):
     # base pointer off by one element and a row stride that is not a multiple of 16 bytes:
