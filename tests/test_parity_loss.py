@@ -249,7 +249,8 @@ def test_unaligned_and_strided_rows(dtype):
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_in_place_dlogits(dtype):
-    T, V = 24, 32000
+    # 3000 rows: several per workgroup, so the bf16 two-buffer kernel swaps its buffers
+    T, V = 3000, 32000
     _say("in_place", dtype, T, V)
     wl = W.make_workload("small_vocab", device=DEV, T=T, V=V, seed=7)
     z = wl.logits.to(dtype)
@@ -359,6 +360,35 @@ def test_forward_only_and_autograd_wrapper():
     (2.0 * loss).backward()
     torch.cuda.synchronize()
     assert torch.allclose(z.grad, 2.0 * both.dlogits, rtol=0, atol=0)
+
+
+@pytest.mark.parametrize("dtype,V", [(torch.bfloat16, 32000), (torch.bfloat16, 2000),
+                                     (torch.float32, 4000), (torch.float32, 32000)])
+def test_forward_only_matches_backward_on_many_short_rows(dtype, V):
+    # the forward-only kernels sum their counters per workgroup like the backward ones:
+    # per-token outputs, the loss and all five counters agree bit for bit
+    T = 5000
+    _say("fwd-only vs fwd+bwd", dtype, T, V)
+    g = torch.Generator(device=DEV).manual_seed(V)
+    z = (torch.randn(T, V, generator=g, device=DEV) * 3).to(dtype)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[3::101] = -1
+    mask = (torch.rand(T, generator=g, device=DEV) > 0.3).to(torch.uint8)
+    lp_ref = torch.randn(T, generator=g, device=DEV) - 8.0
+    lp_mu = lp_ref + 0.5 * torch.randn(T, generator=g, device=DEV)
+    adv = torch.randn(T, generator=g, device=DEV)
+    fwd = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, want_dlogits=False)
+    both = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask)
+    torch.cuda.synchronize()
+    assert torch.equal(fwd.logp.view(torch.int32), both.logp.view(torch.int32))
+    assert torch.equal(fwd.loss_tok, both.loss_tok) and torch.equal(fwd.loss, both.loss)
+    assert torch.equal(fwd.flags, both.flags) and torch.equal(fwd.stats, both.stats)
+    st = both.stats.cpu().numpy()
+    fl = both.flags.cpu().numpy()
+    assert st[0] == int(mask.sum().item())
+    assert st[4] == int(((ids.cpu().numpy() < 0) & (mask.cpu().numpy() != 0)).sum()) > 0
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
 
 
 @pytest.mark.parametrize("kind", ["log_linear", "linear"])
