@@ -322,9 +322,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the loss stage shards by token rows; see the design notes). Run with --gpus 1.",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path (the loss "
+              "stage would shard by token rows, with an all-reduce of five counters). "
+              "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     dev = torch.device("cuda:0")

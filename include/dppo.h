@@ -38,7 +38,7 @@ extern "C" {
 typedef enum {
   DPPO_OK = 0,
   DPPO_ERR_INVALID_ARG = 1, /* null required pointer, bad size, bad enum, bad parameter */
-  DPPO_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+  DPPO_ERR_UNSUPPORTED = 2, /* valid request the library does not implement */
   DPPO_ERR_HIP = 3          /* a HIP runtime call or kernel launch failed */
 } dppo_status;
 

@@ -26,7 +26,7 @@ against the paper:
 * the effective thresholds that interpolation proxies induce on the total ratio
   (Prop. 1; App. A; Table 4).
 
-Readings where the paper is silent (each is listed with its reason in the design notes):
+Readings where the paper is silent, each with its reason:
 
 * The loss value is L = sum_t m_t * s_t * l_t with l_t = -wd_t * min(r_s A, clip(r_s) A),
   s_t = scale * token_scale_t, and scale = loss_scale (constant mode) or

@@ -1,7 +1,7 @@
 """Shared helpers of the GPU parity tests: oracle runs on the same input bits, and the
 comparison rules.
 
-Tolerances (documented with their derivation in the design notes):
+Tolerances, each with the arithmetic it follows from:
   * decisions (band, PPO, flags): bit-exact on every token whose oracle log-ratio is more
     than DELTA = 1e-4 from a threshold (the float32 log-prob error is ~1e-6);
   * lp, lse, l_t: |gpu - ref| <= rtol * max(|ref|, 1), rtol = 1e-5 (fp32 logits) or 2e-3

@@ -368,3 +368,15 @@ def test_versioned_logprob_rejects_null_pointers():
     assert L.logprob_fwd_versioned(None, 2, 1, 4, 8, 8, FAKE, FAKE, FAKE, None, None) == _lib.DPPO_ERR_INVALID_ARG
     # T = 0 is a no-op that touches nothing
     assert L.logprob_fwd_versioned(None, 1, 1, 0, 8, 8, None, None, None, None, None) == _lib.DPPO_OK
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: asked for more it exits with status 2 and says so, before it
+    touches a device."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    p = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300, cwd=root)
+    assert p.returncode == 2, (p.returncode, p.stderr[-500:])
+    assert "one GPU only" in p.stderr and p.stdout == ""
