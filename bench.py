@@ -42,6 +42,7 @@ def log(*a):
 KERNEL_SOURCES = ("dppo_device.h", "loss_stage.h", "token_math.h", "loss_stage.hip")
 SHARD_SOURCES = ("dppo_device.h", "loss_stage.h", "token_math.h", "vocab_shard.h",
                  "vocab_shard.hip")
+EWMA_SOURCES = ("dppo_device.h", "ewma.h", "ewma.hip")
 
 
 def kernel_source_hash(names=KERNEL_SOURCES) -> str:
@@ -156,7 +157,8 @@ def ewma_bandwidth(dev, n, reps=20):
     gbps = 12 * n / (ms * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(gbps / HBM_PEAK_GBPS, 4), "kernel": "dppo::ewma_kernel<false, true>",
-            "n": n, "dtype": "f32", "alg_bytes_per_launch": 12 * n, "kernel_ms": round(ms, 4)}
+            "n": n, "dtype": "f32", "alg_bytes_per_launch": 12 * n, "kernel_ms": round(ms, 4),
+            "traffic": recorded_traffic("ewma_f32_1Gi", EWMA_SOURCES) if n == 1 << 30 else None}
 
 
 def versioned_logprob_measure(dev, wl, K=4, reps=20):
