@@ -20,6 +20,9 @@
  *    dppo_last_error() then describes the failure. A launch failure returns DPPO_ERR_HIP.
  *    Nothing throws across the ABI.
  *  - Data errors are reported on the device, not in the return code (see below).
+ *  - A loss mask ([T] uint8, where a call takes one) is read in aligned 4-byte words, so
+ *    its allocation must be readable up to the next 4-byte boundary past mask + T (true of
+ *    any hipMalloc or PyTorch allocation); the bytes past mask + T are ignored.
  *  - Row strides (`ld`, `ld_dlogits`) are in elements. When a base pointer is not 16-byte
  *    aligned or a stride is not a multiple of 16 bytes, a slower element-wise path runs;
  *    this is not an error.
@@ -329,9 +332,11 @@ typedef struct {
  * both on the device, so that a training step needs no device-to-host copy and no
  * synchronisation (the reset rule of Sec. 5.2 and App. E; the recursion of Eq. 5 / App. B).
  * A one-thread kernel reads the loss stage's counters and updates *state:
- *    rho_t = n_active / n_valid (1 when n_valid = 0; stats NULL means rho_t = 1);
+ *    rho_t = n_active / n_valid (1 when n_valid = 0);
  *    streak <- streak + 1 if rho_t < tau (compared in double), else 0;
  *    a reset fires when streak >= patience; the streak then restarts at 0;
+ *    (stats NULL: rho_t = 1, no reset, the streak unchanged; dppo_reset_decision is the
+ *    same rule on the host)
  *    w_t and (ca, cb) exactly as ewma_proxy_update computes them on the host, in double,
  *    then rounded to float.
  * The element kernel then applies x_prox <- ca x_new + cb x_prox (x_prox not read when
@@ -348,6 +353,31 @@ typedef struct {
 dppo_status ewma_proxy_step(void* x_prox, const void* x_new, int32_t dtype, int64_t n,
                             float beta, double tau, int32_t patience, int32_t normalized,
                             const int32_t* stats, dppo_ewma_state* state, void* stream);
+
+/*
+ * Host side of the PPO-EWMA reference (Sec. 5.2; App. B; App. E). Pure host arithmetic in
+ * double, no HIP call; `stats` here is a HOST copy of the five counters a loss call wrote
+ * (see DPPO_STAT_*). ewma_proxy_step runs the same rule on the device.
+ *
+ * dppo_beta_from_window: the staleness-aware decay beta = W / (W + 2) for a version window
+ *   of width W (App. B), which puts the EWMA's centre of mass beta / (1 - beta) at W / 2.
+ *   INVALID_ARG for W negative or not finite, or a NULL beta.
+ * dppo_train_infer_mask_value: rho_t = n_active / n_valid, the fraction of valid tokens the
+ *   decoupled mask keeps (Sec. 5.2); 1 when no token is valid.
+ * dppo_ppo_clip_ratio: 1 - n_ppo / n_valid, the fraction of valid tokens the PPO clip
+ *   removes; 0 when no token is valid.
+ * dppo_reset_decision: one step of the automatic reset (Sec. 5.2; App. E). *streak (host,
+ *   in/out, >= 0) counts consecutive steps with rho_t < tau, compared in double; *fire = 1
+ *   when the streak reaches `patience` (>= 1), and the streak then restarts at 0. rho
+ *   (nullable) receives rho_t. stats = NULL means no decision input, as in
+ *   ewma_proxy_step: rho_t = 1, no reset, the streak unchanged. tau must be finite. On
+ *   INVALID_ARG nothing is written.
+ */
+dppo_status dppo_beta_from_window(double window, double* beta);
+dppo_status dppo_train_infer_mask_value(const int32_t* stats, double* rho);
+dppo_status dppo_ppo_clip_ratio(const int32_t* stats, double* ratio);
+dppo_status dppo_reset_decision(const int32_t* stats, double tau, int32_t patience,
+                                int32_t* streak, double* rho, int32_t* fire);
 
 /* Row-kernel policy, a testing and benchmarking hook: 0 = automatic (the
  * register-resident kernel when the row fits, the two-pass streaming kernel otherwise),
@@ -383,7 +413,7 @@ const char* dppo_strerror(dppo_status s);
 const char* dppo_last_error(void);
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define DPPO_ABI_VERSION 4
+#define DPPO_ABI_VERSION 5
 int32_t dppo_abi_version(void);
 
 /*

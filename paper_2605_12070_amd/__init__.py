@@ -379,34 +379,48 @@ class KernelTimer:
 
 
 # ------------------------------------------------------------------ host-side controller
+def _host_stats(stats):
+    """The five counters as a host int32 array (a device tensor is copied once)."""
+    if isinstance(stats, torch.Tensor):
+        stats = stats.tolist()
+    vals = [int(v) for v in stats]
+    if len(vals) < _lib.N_STATS:
+        raise ValueError(f"stats must hold {_lib.N_STATS} counters")
+    return (C.c_int32 * _lib.N_STATS)(*vals[:_lib.N_STATS])
+
+
 def beta_from_window(w_stale: float) -> float:
-    """Staleness-aware decay beta = W / (W + 2): the EWMA centre of mass beta / (1 - beta)
-    sits at the middle of a version window of width W (Sec. 5.2; App. B)."""
-    if w_stale < 0:
-        raise ValueError("staleness window must be >= 0")
-    return w_stale / (w_stale + 2.0)
+    """Staleness-aware decay beta = W / (W + 2) (App. B), computed by the library."""
+    out = C.c_double(0.0)
+    _lib.check(_lib.lib().dppo_beta_from_window(float(w_stale), C.byref(out)),
+               "dppo_beta_from_window")
+    return out.value
 
 
 def train_infer_mask_value(stats) -> float:
-    """rho_t = n_active / n_valid (1 when no token is valid)."""
-    n_valid = int(stats[STAT_N_VALID])
-    return 1.0 if n_valid == 0 else int(stats[STAT_N_ACTIVE]) / n_valid
+    """rho_t = n_active / n_valid (1 when no token is valid), computed by the library."""
+    out = C.c_double(0.0)
+    _lib.check(_lib.lib().dppo_train_infer_mask_value(_host_stats(stats), C.byref(out)),
+               "dppo_train_infer_mask_value")
+    return out.value
 
 
 def ppo_clip_ratio(stats) -> float:
-    """Fraction of valid tokens removed by PPO clipping."""
-    n_valid = int(stats[STAT_N_VALID])
-    return 0.0 if n_valid == 0 else 1.0 - int(stats[STAT_N_PPO]) / n_valid
+    """Fraction of valid tokens removed by PPO clipping, computed by the library."""
+    out = C.c_double(0.0)
+    _lib.check(_lib.lib().dppo_ppo_clip_ratio(_host_stats(stats), C.byref(out)),
+               "dppo_ppo_clip_ratio")
+    return out.value
 
 
 class EwmaProxy:
-    """PPO-EWMA reference with automatic reset (Sec. 5.2; App. B; App. E).
+    """PPO-EWMA reference with automatic reset (Sec. 5.2; App. B; App. E), host-driven.
 
     Holds the proxy buffer (parameters or per-token log-probs), the normaliser w and the
-    low-rho streak. `step(x_new, stats)` reads the loss stage's stats (one small
-    device-to-host copy), resets when rho_t < tau has held for `patience` consecutive
-    steps, and otherwise applies the normalised recursion. Its state (buffer, w, streak)
-    is what a checkpoint must save.
+    low-rho streak. `step(x_new, stats)` passes the loss stage's counters (one small
+    device-to-host copy) to the library's reset rule (dppo_reset_decision) and then to
+    ewma_proxy_update, which applies the reset or the normalised recursion. Its state
+    (buffer, w, streak) is what a checkpoint must save.
     """
 
     def __init__(self, x0: torch.Tensor, beta: float, tau: float = 0.9, patience: int = 1,
@@ -424,17 +438,17 @@ class EwmaProxy:
         self.last_rho = 1.0
 
     def decide_reset(self, stats) -> bool:
-        rho = train_infer_mask_value(stats)
-        self.last_rho = rho
-        self.streak = self.streak + 1 if rho < self.tau else 0
-        fire = self.streak >= self.patience
-        if fire:
-            self.streak = 0
-        return fire
+        streak = C.c_int32(self.streak)
+        rho = C.c_double(1.0)
+        fire = C.c_int32(0)
+        _lib.check(_lib.lib().dppo_reset_decision(_host_stats(stats), self.tau, self.patience,
+                                                  C.byref(streak), C.byref(rho), C.byref(fire)),
+                   "dppo_reset_decision")
+        self.streak = streak.value
+        self.last_rho = rho.value
+        return bool(fire.value)
 
     def step(self, x_new: torch.Tensor, stats=None) -> bool:
-        if stats is not None and not isinstance(stats, (list, tuple)):
-            stats = stats.tolist()
         reset = self.decide_reset(stats) if stats is not None else False
         self.w = ewma_proxy_update(self.x, x_new, self.beta, self.w, reset=reset,
                                    normalized=self.normalized)

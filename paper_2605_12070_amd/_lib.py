@@ -21,7 +21,7 @@ STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
 MAX_VERSIONS = 8
 DTYPE_F32, DTYPE_BF16 = 0, 1
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 # Every function the header declares, with its C signature.
 VP, I32, I64, F32, F64 = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double
@@ -66,6 +66,11 @@ SIGNATURES = {
     "logprob_fwd_versioned": (I32, [C.POINTER(VP), I32, I32, I64, I64, I64, VP, VP, VP, VP, VP]),
     "dppo_effective_thresholds": (I32, [C.c_double, C.c_double, C.c_double, C.c_double,
                                         C.c_double, I32, C.POINTER(C.c_double)]),
+    "dppo_beta_from_window": (I32, [F64, C.POINTER(C.c_double)]),
+    "dppo_train_infer_mask_value": (I32, [C.POINTER(I32), C.POINTER(C.c_double)]),
+    "dppo_ppo_clip_ratio": (I32, [C.POINTER(I32), C.POINTER(C.c_double)]),
+    "dppo_reset_decision": (I32, [C.POINTER(I32), F64, I32, C.POINTER(I32),
+                                  C.POINTER(C.c_double), C.POINTER(I32)]),
 }
 
 _lock = threading.Lock()

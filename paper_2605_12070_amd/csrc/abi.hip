@@ -319,6 +319,44 @@ dppo_status dppo_effective_thresholds(double mask_lo, double mask_hi, double cli
   return DPPO_OK;
 }
 
+dppo_status dppo_beta_from_window(double window, double* beta) {
+  if (!beta) return fail(DPPO_ERR_INVALID_ARG, "dppo_beta_from_window: NULL beta");
+  if (!(window >= 0.0) || !std::isfinite(window))
+    return fail(DPPO_ERR_INVALID_ARG, "staleness window %g must be finite and >= 0", window);
+  *beta = window / (window + 2.0);
+  return DPPO_OK;
+}
+
+dppo_status dppo_train_infer_mask_value(const int32_t* stats, double* rho) {
+  if (!stats || !rho) return fail(DPPO_ERR_INVALID_ARG, "dppo_train_infer_mask_value: NULL pointer");
+  *rho = dppo::mask_value(stats);
+  return DPPO_OK;
+}
+
+dppo_status dppo_ppo_clip_ratio(const int32_t* stats, double* ratio) {
+  if (!stats || !ratio) return fail(DPPO_ERR_INVALID_ARG, "dppo_ppo_clip_ratio: NULL pointer");
+  const int32_t nv = stats[DPPO_STAT_N_VALID];
+  *ratio = nv == 0 ? 0.0 : 1.0 - (double)stats[DPPO_STAT_N_PPO] / (double)nv;
+  return DPPO_OK;
+}
+
+dppo_status dppo_reset_decision(const int32_t* stats, double tau, int32_t patience,
+                                int32_t* streak, double* rho, int32_t* fire) {
+  if (!streak || !fire) return fail(DPPO_ERR_INVALID_ARG, "dppo_reset_decision: NULL streak or fire");
+  if (!std::isfinite(tau)) return fail(DPPO_ERR_INVALID_ARG, "tau = %g is not finite", tau);
+  if (patience < 1) return fail(DPPO_ERR_INVALID_ARG, "patience = %d < 1", (int)patience);
+  if (*streak < 0) return fail(DPPO_ERR_INVALID_ARG, "streak = %d < 0", (int)*streak);
+  double r = 1.0;
+  bool f = false;
+  if (stats) {
+    r = dppo::mask_value(stats);
+    f = dppo::reset_rule(r, tau, patience, streak);
+  }
+  if (rho) *rho = r;
+  *fire = f ? 1 : 0;
+  return DPPO_OK;
+}
+
 dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                         const int64_t* token_ids, float* logp_out, float* lse_out, void* stream) {
   dppo_status s = check_matrix(logits, dtype, T, V, ld, "logits");
@@ -600,19 +638,7 @@ dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, in
 
   // Coefficients of x_prox <- ca * x_new + cb * x_prox, in double on the host.
   double ca, cb, w_new = normalized ? *w : 0.0;
-  if (reset) {
-    ca = 1.0;
-    cb = 0.0;
-    if (normalized) w_new = 1.0;
-  } else if (normalized) {
-    const double wp = *w;
-    w_new = 1.0 + (double)beta * wp;
-    ca = 1.0 / w_new;
-    cb = (double)beta * wp / w_new;
-  } else {
-    ca = 1.0 - (double)beta;
-    cb = (double)beta;
-  }
+  dppo::ewma_coefficients(reset != 0, normalized != 0, (double)beta, &w_new, &ca, &cb);
   if (n > 0) {
     const bool aligned = aligned16(x_prox) && aligned16(x_new);
     const hipError_t e = dppo::launch_ewma(x_prox, x_new, dtype == DPPO_BF16, n, (float)ca,

@@ -118,9 +118,11 @@ __device__ __forceinline__ void wave_merge_ns_int(float& n, float& s) {
 }
 
 // Workgroup-wide merge of integer-shift partials with a single barrier. `lds` holds
-// 2 * (NT / 64) floats and must not be reused by the workgroup before its next barrier
-// (callers alternate two buffers). Every thread returns the same bits: each wave merges
-// the NT / 64 wave results in the same fixed tree.
+// 2 * (NT / 64) floats and must not be written again before the workgroup's next barrier:
+// callers alternate two buffers from one merge to the next (not by row: a row that runs no
+// merge must not flip the buffer, or two merges in a row would share one with no barrier
+// between them). Every thread returns the same bits: each wave merges the NT / 64 wave
+// results in the same fixed tree.
 template <int NT>
 __device__ __forceinline__ void block_merge_ns_int(float& n, float& s, float* lds) {
   constexpr int NW = NT / 64;
@@ -172,8 +174,9 @@ __device__ __forceinline__ T uload(const T* p) {
 }
 
 // A uniform byte through the scalar unit, which has no byte loads: the aligned 32-bit word
-// holding the byte (same page, so always mapped) is loaded and shifted. A plain byte load
-// would become a vector load.
+// holding the byte is loaded and shifted. A plain byte load would become a vector load. The
+// word can reach up to 3 bytes past the last mask byte; the ABI therefore asks for a mask
+// allocation readable up to the next 4-byte boundary (every device allocation is).
 __device__ __forceinline__ uint32_t uload_u8(const uint8_t* p) {
   const uintptr_t a = (uintptr_t)p;
   const uint32_t w = uload((const uint32_t*)(a & ~(uintptr_t)3));

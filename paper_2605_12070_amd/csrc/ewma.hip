@@ -115,29 +115,12 @@ __global__ __launch_bounds__(64) void ewma_controller(const int32_t* stats, dppo
   double rho = 1.0;
   bool fire = false;
   if (stats != nullptr) {
-    const int32_t nv = stats[DPPO_STAT_N_VALID];
-    rho = nv == 0 ? 1.0 : (double)stats[DPPO_STAT_N_ACTIVE] / (double)nv;
-    st.streak = rho < tau ? st.streak + 1 : 0;
-    fire = st.streak >= patience;
-    if (fire) {
-      st.streak = 0;
-      st.resets += 1;
-    }
+    rho = mask_value(stats);
+    fire = reset_rule(rho, tau, patience, &st.streak);
+    if (fire) st.resets += 1;
   }
   double ca, cb;
-  if (fire) {
-    ca = 1.0;
-    cb = 0.0;
-    if (normalized) st.w = 1.0;
-  } else if (normalized) {
-    const double wp = st.w;
-    st.w = 1.0 + (double)beta * wp;
-    ca = 1.0 / st.w;
-    cb = (double)beta * wp / st.w;
-  } else {
-    ca = 1.0 - (double)beta;
-    cb = (double)beta;
-  }
+  ewma_coefficients(fire, normalized != 0, (double)beta, &st.w, &ca, &cb);
   st.last_reset = fire ? 1 : 0;
   st.error = 0;
   st.last_rho = (float)rho;

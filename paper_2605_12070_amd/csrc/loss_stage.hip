@@ -147,7 +147,7 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 // ---------------------------------------------------------------------------------------
 template <int NT, int NC, bool BWD, bool DB>
 __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
-  __shared__ float red[2][2 * (NT / 64)];   // alternated by row parity: one barrier per merge
+  __shared__ float red[2][2 * (NT / 64)];   // alternated merge by merge: one barrier per merge
   __shared__ Bcast bc;
   // Per-chunk shifts n_c live in LDS (NC x NT floats, conflict-free [c][tid] layout): the
   // registers are reserved for the row itself.
@@ -269,6 +269,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
       float n = N;
       float s = S;
       block_merge_ns_int<NT>(n, s, red[parity]);
+      parity ^= 1;                          // the buffers alternate between merges
       // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
       const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
       finish_row(a, row, zy, lse2, good, &bc, tin, sc);
@@ -350,15 +351,13 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
       step(r1, r2, first);
       first = false;
       row += gridDim.x;
-      parity ^= 1;
       if (row >= a.T) break;
       step(r2, r1, false);
       row += gridDim.x;
-      parity ^= 1;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the loads past the last row
   } else {
-    for (; row < a.T; row += gridDim.x, parity ^= 1) step(r1, r1, false);
+    for (; row < a.T; row += gridDim.x) step(r1, r1, false);
   }
   if (threadIdx.x == 0) flush_stats(a, sc);
 }
@@ -407,8 +406,8 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
   }
-  int parity = 0;
-  for (; row < a.T; row += gridDim.x, parity ^= 1) {
+  int parity = 0;                          // flips after each merge that ran
+  for (; row < a.T; row += gridDim.x) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     const int tid = threadIdx.x;
     const int V = a.V;
@@ -457,6 +456,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
     }
     if (rd_cur) {
       block_merge_ns_int<NT>(N, S, red[parity]);
+      parity ^= 1;
       const float lse2 = (N == -INFINITY) ? __builtin_nanf("") : N + log2f(S);
       finish_row(a, row, zy, lse2, good, &bc, tin, sc);
     } else if (tid == 0) {                  // masked row, or a bad id on a valid loss row

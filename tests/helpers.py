@@ -8,9 +8,16 @@ Tolerances, each with the arithmetic it follows from:
     (bf16 logits) as the contract states, and a tight implementation bound TIGHT = 2e-5
     that a dropped or doubled vocabulary element would break;
   * scalar loss: |gpu - ref| <= 1e-5 * sum_t |m_t s_t l_t| + 1e-30;
-  * dlogits: |gpu - ref| <= DREL * |ref| + 1e-5 * |w_t| per element, DREL = 2^-7 for bf16
-    output (one bf16 ulp; fp16-stored exponentials add <= 2^-11) and 2e-5 for fp32 output;
-    plus the contract's absolute bound 1e-3 on bf16 dlogits.
+  * dlogits: |gpu - ref| <= DREL * |ref| + 2^-22 * |w_t| per element. For bf16 output
+    DREL = 2^-8 + 2^-11: rounding to nearest bf16 (8 significant bits) is off by at most
+    2^-8 |ref|, and the exponentials the resident kernels keep as fp16 (11 significant
+    bits) add at most 2^-11 before that rounding. The floor covers exponentials in fp16's
+    subnormal range, absolute error <= 2^-25 each, scaled by w_t 2^(n_c - lse2) < 2 w_t:
+    <= 2^-24 |w_t|, with a factor 4 to spare. For fp32 output DREL = 2e-5 (the fp32
+    log-sum-exp's error, ~1e-6, moves every softmax entry by that much relatively). Plus
+    the contract's absolute bound 1e-3 on bf16 dlogits wherever a correctly rounded value
+    can meet it: |ref| <= 1/4, where half a bf16 ulp is <= 2^-11 and the fp16 step adds
+    <= 2^-13.
 """
 from __future__ import annotations
 
@@ -73,8 +80,8 @@ def assert_close_rel(gpu, ref, rtol, what, floor=1.0, mask=None):
 
 def check_dlogits_rows(gpu_rows, ref_rows, w, out_dtype, what="dlogits"):
     """gpu_rows: float64 values of the kernel's dlogits rows; ref_rows: oracle float64."""
-    drel = 2.0 ** -7 if out_dtype == torch.bfloat16 else 2e-5
-    bound = drel * np.abs(ref_rows) + 1e-5 * np.abs(w)[:, None] + 1e-30
+    drel = 2.0 ** -8 + 2.0 ** -11 if out_dtype == torch.bfloat16 else 2e-5
+    bound = drel * np.abs(ref_rows) + 2.0 ** -22 * np.abs(w)[:, None] + 1e-30
     nan_ref = np.isnan(ref_rows)
     assert np.array_equal(np.isnan(gpu_rows), nan_ref), f"{what}: NaN pattern differs"
     err = np.where(nan_ref, 0.0, np.abs(gpu_rows - ref_rows))
@@ -82,9 +89,8 @@ def check_dlogits_rows(gpu_rows, ref_rows, w, out_dtype, what="dlogits"):
     assert not bad.any(), (f"{what}: {int(bad.sum())} elements out of bound, worst excess "
                            f"{float((err - bound).max()):.3e}")
     if out_dtype == torch.bfloat16:
-        # The contract's absolute bound. Above |ref| = 1/8 one bf16 ulp alone exceeds 1e-3,
-        # so the bound applies where a correctly rounded value can meet it.
-        small = np.abs(np.where(nan_ref, 0.0, ref_rows)) <= 0.125
+        # The contract's absolute bound, where a correctly rounded value can meet it.
+        small = np.abs(np.where(nan_ref, 0.0, ref_rows)) <= 0.25
         worst = float(np.max(np.where(small, err, 0.0), initial=0.0))
         assert worst <= 1e-3, f"{what}: absolute error {worst:.3e} > 1e-3"
 

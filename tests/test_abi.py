@@ -217,6 +217,89 @@ def test_host_controller_logic():
     assert P.train_infer_mask_value([10, 9, 9, 8, 0]) == 0.8
     assert P.train_infer_mask_value([0, 0, 0, 0, 0]) == 1.0
     assert abs(P.ppo_clip_ratio([10, 9, 7, 6, 0]) - 0.3) < 1e-12
+    assert P.ppo_clip_ratio([0, 0, 0, 0, 0]) == 0.0
+
+
+def test_host_controller_exports_match_the_oracle():
+    """The a9 arithmetic lives in the library (dppo_beta_from_window, dppo_*_value,
+    dppo_reset_decision), called here through ctypes on the CPU, against the oracle's
+    definitions: beta = W / (W + 2) with centre of mass W / 2 (App. B), rho_t and the clip
+    ratio from the counters, and the reset schedule over seeded rho sequences (Sec. 5.2;
+    App. E) for several patiences and thresholds."""
+    import numpy as np
+    from oracle import dppo_oracle as oracle
+    L = _lib.lib()
+    out = C.c_double(0.0)
+    for W in (0.0, 0.5, 1, 2, 3, 6, 10, 1e6):
+        assert L.dppo_beta_from_window(float(W), C.byref(out)) == _lib.DPPO_OK
+        assert out.value == oracle.beta_from_window(W)
+        if W > 0:
+            assert abs(oracle.ewma_center_of_mass(out.value) - W / 2) <= 1e-9 * max(1.0, W)
+    for bad in (-1.0, float("inf"), float("nan")):
+        assert L.dppo_beta_from_window(bad, C.byref(out)) == _lib.DPPO_ERR_INVALID_ARG
+    assert L.dppo_beta_from_window(1.0, None) == _lib.DPPO_ERR_INVALID_ARG
+
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        nv = int(rng.integers(0, 5000))
+        nb, np_ = (int(rng.integers(0, nv + 1)) for _ in range(2))
+        na = int(rng.integers(0, min(nb, np_) + 1))
+        st = [nv, nb, np_, na, int(rng.integers(0, 3))]
+        arr = (C.c_int32 * 5)(*st)
+        assert L.dppo_train_infer_mask_value(arr, C.byref(out)) == _lib.DPPO_OK
+        assert out.value == oracle.train_infer_mask_value(st)
+        assert L.dppo_ppo_clip_ratio(arr, C.byref(out)) == _lib.DPPO_OK
+        assert out.value == oracle.ppo_clip_ratio(st)
+
+    for tau, patience, seed in ((0.9, 1, 0), (0.9, 2, 1), (0.8, 3, 2), (0.95, 1, 3)):
+        r = np.random.default_rng(seed)
+        n_valid = 1000
+        actives = r.integers(700, 1001, size=60)
+        stats = [[n_valid, n_valid, n_valid, int(a), 0] for a in actives]
+        stats[7] = [0, 0, 0, 0, 0]                       # no valid token: rho = 1
+        rhos = [oracle.train_infer_mask_value(s) for s in stats]
+        want = oracle.reset_schedule(rhos, tau=tau, patience=patience)
+        streak = C.c_int32(0)
+        rho = C.c_double(0.0)
+        fire = C.c_int32(0)
+        got = []
+        for s_, rho_want in zip(stats, rhos):
+            arr = (C.c_int32 * 5)(*s_)
+            assert L.dppo_reset_decision(arr, tau, patience, C.byref(streak), C.byref(rho),
+                                         C.byref(fire)) == _lib.DPPO_OK
+            assert rho.value == rho_want
+            got.append(bool(fire.value))
+        assert got == list(want), (tau, patience)
+        assert any(want) and not all(want)
+    # stats = NULL: no decision input, as in ewma_proxy_step: no reset, streak unchanged
+    streak = C.c_int32(3)
+    assert L.dppo_reset_decision(None, 0.9, 5, C.byref(streak), None, C.byref(fire)) == _lib.DPPO_OK
+    assert fire.value == 0 and streak.value == 3
+    arr = (C.c_int32 * 5)(10, 10, 10, 1, 0)
+    for kw in (dict(tau=float("nan")), dict(patience=0), dict(streak=-1)):
+        a = dict(tau=0.9, patience=1, streak=0)
+        a.update(kw)
+        sk = C.c_int32(a["streak"])
+        assert L.dppo_reset_decision(arr, a["tau"], a["patience"], C.byref(sk), None,
+                                     C.byref(fire)) == _lib.DPPO_ERR_INVALID_ARG
+
+
+def test_host_ewma_proxy_decisions_follow_the_library(monkeypatch):
+    """EwmaProxy.decide_reset keeps only the streak and passes the counters through: its
+    decisions equal the oracle's schedule (no GPU: the buffer update is not called)."""
+    import paper_2605_12070_amd as P
+    from oracle import dppo_oracle as oracle
+
+    class _NoBuf:
+        def clone(self):
+            return self
+
+    px = P.EwmaProxy(_NoBuf(), beta=0.75, tau=0.9, patience=2)
+    stats = [[100, 100, 100, a, 0] for a in (95, 85, 80, 99, 70, 60, 50, 91, 89, 88)]
+    want = oracle.reset_schedule([oracle.train_infer_mask_value(s) for s in stats], 0.9, 2)
+    got = [px.decide_reset(s) for s in stats]
+    assert got == list(want)
+    assert px.last_rho == 0.88
 
 
 def test_row_kernel_name_follows_the_selection_rule():

@@ -69,6 +69,46 @@ def _check_workload(wl, lp_ref, lp_mu, oracle_lp_ref, n_rand=48):
     return res
 
 
+def test_large_vocab_flagship_several_rows_per_workgroup():
+    """The flagship kernel (bf16, V = 151936, 1024 threads x 19 chunks) in its persistent
+    mode, element by element: T = 1024 rows on a grid of at most 216 workgroups gives every
+    workgroup 4-5 rows, with the staggered start on (T >= 4 x grid) and the next row's loads
+    issued after this row's stores. About 10 % of rows are masked and some valid rows carry
+    bad ids, so rows that are not read sit between rows that are. Every row of lp, loss_tok,
+    flags and dlogits is compared with the oracle (in blocks of rows, float64)."""
+    T, V = 1024, 151936
+    print(f"[case] flagship multi-row T={T} V={V}", flush=True)
+    wl = W.make_workload("large_vocab", device=DEV, T=T, seed=21, seq_len=128)
+    assert P.row_kernel_name(torch.bfloat16, V) == "dppo::rows_bf16_resident<1024, 19, true>"
+    g = torch.Generator(device=DEV).manual_seed(21)
+    mask = (torch.rand(T, generator=g, device=DEV) >= 0.1).to(torch.uint8)
+    ids = wl.ids.clone()
+    ids[3::53] = V                                      # bad ids (on valid and masked rows)
+    ids[29::211] = -1
+    anchor = torch_anchor(wl.logits, ids.clamp(0, V - 1))
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    res = P.decoupled_ppo_loss_fwd_bwd(wl.logits, ids, lp_mu, lp_ref, wl.adv, mask)
+    torch.cuda.synchronize()
+    m = mask.cpu().numpy()
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    scale = oracle.batch_scale(m, params)
+    ids_np = ids.cpu().numpy()
+    for a in range(0, T, 128):
+        rows = np.arange(a, min(T, a + 128))
+        idx = torch.as_tensor(rows, device=DEV)
+        ref = oracle.per_token(bits_of(wl.logits[idx]), ids_np[rows],
+                               lp_mu[idx].cpu().double().numpy(),
+                               lp_ref[idx].cpu().double().numpy(),
+                               wl.adv[idx].cpu().double().numpy(), m[rows], None, params, scale)
+        compare_loss(res, ref, params, torch.bfloat16, rows=rows)
+    fl = res.flags.cpu().numpy()
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
+    bad = ((ids_np < 0) | (ids_np >= V)) & (m != 0)
+    assert st[0] == int(m.sum()) and st[4] == int(bad.sum()) > 0
+    assert (m == 0).sum() > 50
+
+
 def test_large_vocab_fullsize():
     wl = W.make_workload("large_vocab", device=DEV)
     anchor = torch_anchor(wl.logits, wl.ids)
