@@ -194,26 +194,34 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
  * fused_lm_head_loss_fwd_bwd -- decoupled_ppo_loss_fwd_bwd on logits z = hidden weight^T
  * that are never written to memory, with the gradients of L for both factors:
  *     d L / d hidden = G weight,   d L / d weight = G^T hidden,
- *     G[t, v] = w_t (softmax(z_t)[v] - 1{v = y_t})   (the dlogits of the row entry point).
- * The logits exist only as 128 x 128 tiles in registers and LDS, formed with bf16 matrix-core
- * products and fp32 accumulation; the forward pass reduces each tile to a per-token partial
- * log-sum-exp, the backward pass recomputes the tiles and writes G in bf16 one vocabulary
- * chunk at a time into the workspace, and the two gradient products (plain GEMMs, fp32
- * results) run in rocBLAS. lp, loss, flags, stats and the parameters are as in
- * decoupled_ppo_loss_fwd_bwd (ref_mode included).
+ *     G[t, v] = w_t (softmax(z_t)[v] - 1{v = y_t})   (the dlogits of the row entry point,
+ *     the MIS gradient of Sec. 3.1 chained through the LM head).
+ * The logits exist only as 256 x 256 tiles in registers and LDS, formed with bf16
+ * matrix-core products and fp32 accumulation; the forward pass reduces each tile to
+ * per-token partial log-sum-exps. All four products run in the library's own matrix-core
+ * kernels. lp, loss, flags, stats and the parameters are as in decoupled_ppo_loss_fwd_bwd
+ * (ref_mode included).
+ *
+ * Two ways to form G, chosen by vocab_chunk:
+ *  - vocab_chunk <= 0 or >= V (one pass, the default): the forward tiles also store their
+ *    exponentials 2^(z log2 e - m) (m the maximum of each 128-entry vocabulary group) as
+ *    fp16 into the workspace; once every token's log-sum-exp is known, a row pass scales
+ *    them into G in bf16 in place. The logits are formed once.
+ *  - 0 < vocab_chunk < V (chunked, for a smaller workspace): the backward recomputes the
+ *    logit tiles one vocabulary chunk at a time and writes that chunk of G in bf16; the two
+ *    gradient products then run on the chunk. The logits are formed twice.
  *
  *  hidden       [T, d] bf16, row-major, 16-byte aligned.
  *  weight       [V, d] bf16, row-major (an LM head in the [out, in] layout), 16-byte aligned.
  *  dtype        DPPO_BF16 (DPPO_F32 is DPPO_ERR_UNSUPPORTED).
- *  d            multiple of 8, at most 2^20; V < 2^23; T < 2^31.
+ *  d            multiple of 8, at most 2^20; 1 <= V <= 2^21; T < 2^31.
  *  dhidden      [T, d] float32 or NULL (not computed); overwritten.
  *  dweight      [V, d] float32 or NULL (not computed); overwritten.
- *  vocab_chunk  vocabulary rows per backward chunk (rounded up to 128); <= 0 means all of V.
+ *  vocab_chunk  see above; a chunk is rounded up to a multiple of 256 vocabulary rows.
  *  workspace    device buffer of at least fused_lm_head_workspace_bytes(T, d, V, vocab_chunk)
  *               bytes, 256-byte aligned, owned by the caller; its contents are scratch.
  * Masked rows and bad ids behave as in the row entry point (their G rows are zero). The
- * computation of rows with loss mask 0 is not skipped. rocBLAS is initialised on the first
- * call on a device (one handle per device, kept for the process).
+ * computation of rows with loss mask 0 is not skipped. The call allocates nothing.
  */
 dppo_status fused_lm_head_loss_fwd_bwd(
     const void* hidden, const void* weight, int32_t dtype, int64_t T, int64_t d, int64_t V,
@@ -224,8 +232,9 @@ dppo_status fused_lm_head_loss_fwd_bwd(
     int64_t vocab_chunk, void* workspace, int64_t workspace_bytes, void* stream);
 
 /* Workspace bytes fused_lm_head_loss_fwd_bwd needs for these sizes (-1 if they are out of
- * range): per-token partial sums of every 128-entry vocabulary tile (8 B per token and
- * tile), four per-token vectors and one bf16 [T, vocab_chunk] gradient chunk. */
+ * range): per-token partial sums of every 128-entry vocabulary group (8 B per token and
+ * group), four per-token vectors, and either [T, V rounded up to 256] of 2 bytes (one
+ * pass) or one bf16 [T, chunk] gradient chunk (chunked). */
 int64_t fused_lm_head_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t vocab_chunk);
 
 /*
@@ -420,9 +429,9 @@ int32_t dppo_abi_version(void);
  * Kernel timer for profiling. While enabled, the library records a pair of HIP events on
  * the call's stream around every launch of the per-row loss-stage kernel (the one that
  * streams the logits; for the vocabulary-shard calls, the shard kernel; for the fused LM
- * head, its two tile kernels) and, on dppo_timer_read, synchronises those events and returns the
- * summed elapsed time in milliseconds and the number of launches timed, then clears the
- * record. Enabling allocates host-side event objects; it is process-global state, meant
+ * head, its logit-tile kernels and each gradient product) and, on dppo_timer_read,
+ * synchronises those events and returns the summed elapsed time in milliseconds and the
+ * number of launches timed, then clears the record. Enabling allocates host-side event objects; it is process-global state, meant
  * for one profiling thread.
  */
 dppo_status dppo_timer_enable(int32_t on);

@@ -21,7 +21,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdppo.so")
-SOURCES = ["loss_stage.hip", "lm_head.hip", "ewma.hip", "vocab_shard.hip", "abi.hip"]
+SOURCES = ["loss_stage.hip", "lm_head.hip", "lm_head_grad.hip", "ewma.hip", "vocab_shard.hip",
+           "abi.hip"]
 ARCH = "gfx950"
 
 FLAGS = [
@@ -31,9 +32,8 @@ FLAGS = [
 ]
 
 
-ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
-# rocBLAS runs the two plain gradient GEMMs of the fused LM head
-LINK = [f"-L{ROCM}/lib", "-lrocblas", f"-Wl,-rpath,{ROCM}/lib"]
+# The library links nothing beyond the HIP runtime that hipcc adds.
+LINK: list[str] = []
 
 
 def hipcc() -> str:

@@ -16,7 +16,6 @@
 #include "vocab_shard.h"
 #include "loss_stage.h"
 
-#include <rocblas/rocblas.h>
 
 namespace {
 
@@ -141,48 +140,34 @@ dppo_status check_matrix(const void* p, int32_t dtype, int64_t T, int64_t V, int
   return DPPO_OK;
 }
 
-// One rocBLAS handle per device, created on first use and kept for the process.
-rocblas_status blas_handle(rocblas_handle* out) {
-  static std::mutex mu;
-  static std::vector<std::pair<int, rocblas_handle>> handles;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return rocblas_status_internal_error;
-  std::lock_guard<std::mutex> lk(mu);
-  for (auto& h : handles)
-    if (h.first == dev) {
-      *out = h.second;
-      return rocblas_status_success;
-    }
-  rocblas_handle h = nullptr;
-  const rocblas_status st = rocblas_create_handle(&h);
-  if (st != rocblas_status_success) return st;
-  handles.push_back({dev, h});
-  *out = h;
-  return rocblas_status_success;
-}
-
 struct LmhLayout {
   int64_t part, zy, w, lse2, ev, g, total;  // byte offsets into the workspace, and its size
   int64_t chunk, ldg;                        // vocabulary rows per backward chunk, g's stride
+  bool one_pass;                             // G from the forward tiles' exponentials
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
+// Workspace of the fused LM head. With vocab_chunk <= 0 or >= V (one pass) g holds the
+// forward tiles' fp16 exponentials for the whole vocabulary, [T, ldg] with ldg = V rounded
+// up to the tile width, and becomes G in place; otherwise g holds one bf16 chunk of G,
+// [T, chunk] with chunk rounded up to the tile width.
 LmhLayout lmh_layout(int64_t T, int64_t V, int64_t vocab_chunk) {
   LmhLayout L;
-  const int64_t ntiles = (V + dppo::LMH_BN - 1) / dppo::LMH_BN;
-  int64_t chunk = vocab_chunk <= 0 ? V : vocab_chunk;
-  chunk = ((chunk + dppo::LMH_BN - 1) / dppo::LMH_BN) * dppo::LMH_BN;
-  if (chunk > ntiles * dppo::LMH_BN) chunk = ntiles * dppo::LMH_BN;
-  L.chunk = chunk;
+  const int64_t ngroups = dppo::lmh_groups((int)V);
+  const int64_t vpad = ((V + dppo::LMH_BN - 1) / dppo::LMH_BN) * dppo::LMH_BN;
+  L.one_pass = vocab_chunk <= 0 || vocab_chunk >= V;
+  int64_t chunk = L.one_pass ? vpad : ((vocab_chunk + dppo::LMH_BN - 1) / dppo::LMH_BN) * dppo::LMH_BN;
+  if (chunk > vpad) chunk = vpad;
+  L.chunk = L.one_pass ? V : chunk;
   L.ldg = chunk;
   int64_t o = 0;
-  L.part = o; o = align256(o + ntiles * T * 2 * 4);
+  L.part = o; o = align256(o + ngroups * T * 2 * 4);
   L.zy = o;   o = align256(o + T * 4);
   L.w = o;    o = align256(o + T * 4);
   L.lse2 = o; o = align256(o + T * 4);
   L.ev = o;   o = align256(o + T);
-  L.g = o;    o = align256(o + T * chunk * 2);
+  L.g = o;    o = align256(o + T * L.ldg * 2);
   L.total = o;
   return L;
 }
@@ -481,7 +466,7 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
 }
 
 int64_t fused_lm_head_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t vocab_chunk) {
-  if (T < 0 || d < 8 || V < 1 || T >= ((int64_t)1 << 31) || V >= ((int64_t)1 << 31)) return -1;
+  if (T < 0 || d < 8 || V < 1 || T >= ((int64_t)1 << 31) || V > ((int64_t)1 << 21)) return -1;
   return lmh_layout(T, V, vocab_chunk).total;
 }
 
@@ -497,7 +482,7 @@ dppo_status fused_lm_head_loss_fwd_bwd(
   if (dtype != DPPO_BF16)
     return fail(DPPO_ERR_UNSUPPORTED, "the fused LM head takes bf16 hidden states and weights");
   if (T < 0 || T >= ((int64_t)1 << 31)) return fail(DPPO_ERR_INVALID_ARG, "T = %lld out of range", (long long)T);
-  if (V < 1 || V >= ((int64_t)1 << 23)) return fail(DPPO_ERR_INVALID_ARG, "V = %lld out of range", (long long)V);
+  if (V < 1 || V > ((int64_t)1 << 21)) return fail(DPPO_ERR_INVALID_ARG, "V = %lld out of [1, 2^21]", (long long)V);
   if (d < 8 || d % 8 != 0 || d > (1 << 20))
     return fail(DPPO_ERR_INVALID_ARG, "d = %lld must be a multiple of 8 in [8, 2^20]", (long long)d);
   if (!p) return fail(DPPO_ERR_INVALID_ARG, "params pointer is NULL");
@@ -513,11 +498,6 @@ dppo_status fused_lm_head_loss_fwd_bwd(
                 (long long)workspace_bytes);
   if (T > 0 && ((uintptr_t)workspace & 255u))
     return fail(DPPO_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
-  rocblas_handle blas = nullptr;
-  if ((dhidden || dweight) && T > 0) {
-    if (blas_handle(&blas) != rocblas_status_success)
-      return fail(DPPO_ERR_HIP, "rocBLAS handle creation failed");
-  }
   hipStream_t st = (hipStream_t)stream;
   dppo::launch_prep_stats(loss_mask, T, stats_out, st);
   hipError_t e = hipGetLastError();
@@ -526,6 +506,7 @@ dppo_status fused_lm_head_loss_fwd_bwd(
     if (dweight && (e = dppo::launch_lmh_zero(dweight, V * d, st)) != hipSuccess)
       return hip_fail(e, "zero fill");
   } else {
+    const bool grads = dhidden || dweight;
     char* ws = (char*)workspace;
     dppo::LmhArgs m{};
     m.hidden = (const uint16_t*)hidden;
@@ -543,6 +524,7 @@ dppo_status fused_lm_head_loss_fwd_bwd(
     m.ids = token_ids;
     m.g = (uint16_t*)(ws + L.g);
     m.ldg = L.ldg;
+    m.store_p = grads && L.one_pass;
     dppo::RowArgs a{};
     a.ids = token_ids;
     a.lp_mu = logp_mu_old;
@@ -566,50 +548,72 @@ dppo_status fused_lm_head_loss_fwd_bwd(
     a.scale_mode = p->scale_mode;
     a.ref_mode = p->ref_mode;
     a.alpha = p->alpha;
+    // timed launches: the forward tiles and each gradient product
+    auto timed = [&](auto&& launch) -> hipError_t {
+      auto* ev = timer_slot();
+      if (ev) (void)hipEventRecord(ev->first, st);
+      const hipError_t le = launch();
+      if (ev) (void)hipEventRecord(ev->second, st);
+      return le;
+    };
+    // dhidden (+)= G_c W_c over the chunk's vocabulary rows [n0, n1) (K = n1 - n0), and
+    // dweight rows [n0, n1) = G_c^T hidden (K = T); G_c is [T, ldg] bf16 in the workspace.
+    auto products = [&](int64_t n0, int64_t n1) -> dppo_status {
+      const int64_t kc = n1 - n0;
+      if (dhidden) {
+        dppo::GemmArgs g{};
+        g.a = m.g;
+        g.lda = L.ldg;
+        g.a_ext = (int32_t)T;
+        g.b = (const uint16_t*)weight + n0 * d;
+        g.ldb = d;
+        g.b_ext = (int32_t)d;
+        g.M = (int32_t)T;
+        g.N = (int32_t)d;
+        g.K = (int32_t)kc;
+        g.c = dhidden;
+        g.ldc = d;
+        g.accumulate = n0 > 0;
+        if ((e = timed([&] { return dppo::launch_lmh_grad_gemm(g, false, true, st); })) != hipSuccess)
+          return hip_fail(e, "dhidden product launch");
+      }
+      if (dweight) {
+        dppo::GemmArgs g{};
+        g.a = m.g;
+        g.lda = L.ldg;
+        g.a_ext = (int32_t)((kc + 7) & ~(int64_t)7);
+        g.b = (const uint16_t*)hidden;
+        g.ldb = d;
+        g.b_ext = (int32_t)d;
+        g.M = (int32_t)kc;
+        g.N = (int32_t)d;
+        g.K = (int32_t)T;
+        g.c = dweight + n0 * d;
+        g.ldc = d;
+        g.accumulate = 0;
+        if ((e = timed([&] { return dppo::launch_lmh_grad_gemm(g, true, true, st); })) != hipSuccess)
+          return hip_fail(e, "dweight product launch");
+      }
+      return DPPO_OK;
+    };
     if ((e = dppo::launch_lmh_zy(m, st)) != hipSuccess) return hip_fail(e, "z_y launch");
-    auto* ev = timer_slot();
-    if (ev) (void)hipEventRecord(ev->first, st);
-    e = dppo::launch_lmh_fwd_tiles(m, st);
-    if (ev) (void)hipEventRecord(ev->second, st);
-    if (e != hipSuccess) return hip_fail(e, "forward tile launch");
-    if ((e = dppo::launch_lmh_finish(a, m, st)) != hipSuccess) return hip_fail(e, "finish launch");
-    if (dhidden || dweight) {
-      if (rocblas_set_stream(blas, st) != rocblas_status_success)
-        return fail(DPPO_ERR_HIP, "rocblas_set_stream failed");
-      const float one = 1.0f, zero = 0.0f;
-      for (int64_t n0 = 0; n0 < V; n0 += L.chunk) {
+    if ((e = timed([&] { return dppo::launch_lmh_fwd_tiles(m, st); })) != hipSuccess)
+      return hip_fail(e, "forward tile launch");
+    if (m.store_p) {
+      // one pass: the row pass finishes every token and forms G in place
+      if ((e = dppo::launch_lmh_grad_rows(a, m, st)) != hipSuccess) return hip_fail(e, "gradient row launch");
+      s = products(0, V);
+      if (s != DPPO_OK) return s;
+    } else {
+      if ((e = dppo::launch_lmh_finish(a, m, st)) != hipSuccess) return hip_fail(e, "finish launch");
+      for (int64_t n0 = 0; grads && n0 < V; n0 += L.chunk) {
         const int64_t n1 = std::min<int64_t>(V, n0 + L.chunk);
         m.n0 = (int32_t)n0;
         m.n1 = (int32_t)n1;
-        auto* evb = timer_slot();
-        if (evb) (void)hipEventRecord(evb->first, st);
-        e = dppo::launch_lmh_bwd_tiles(m, st);
-        if (evb) (void)hipEventRecord(evb->second, st);
-        if (e != hipSuccess) return hip_fail(e, "backward tile launch");
-        const rocblas_int kc = (rocblas_int)(n1 - n0);
-        rocblas_status bs;
-        if (dhidden) {
-          // column-major view: dhidden^T [d x T] (+)= weight_c^T [d x kc] . g^T [kc x T]
-          bs = rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_none,
-                               (rocblas_int)d, (rocblas_int)T, kc, &one,
-                               (const uint16_t*)weight + n0 * d, rocblas_datatype_bf16_r, (rocblas_int)d,
-                               m.g, rocblas_datatype_bf16_r, (rocblas_int)L.ldg,
-                               n0 == 0 ? &zero : &one, dhidden, rocblas_datatype_f32_r, (rocblas_int)d,
-                               dhidden, rocblas_datatype_f32_r, (rocblas_int)d,
-                               rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
-          if (bs != rocblas_status_success) return fail(DPPO_ERR_HIP, "rocBLAS dhidden GEMM failed (%d)", (int)bs);
-        }
-        if (dweight) {
-          // column-major view: dweight_c^T [d x kc] = hidden^T [d x T] . g [T x kc]
-          bs = rocblas_gemm_ex(blas, rocblas_operation_none, rocblas_operation_transpose,
-                               (rocblas_int)d, kc, (rocblas_int)T, &one,
-                               hidden, rocblas_datatype_bf16_r, (rocblas_int)d,
-                               m.g, rocblas_datatype_bf16_r, (rocblas_int)L.ldg,
-                               &zero, dweight + n0 * d, rocblas_datatype_f32_r, (rocblas_int)d,
-                               dweight + n0 * d, rocblas_datatype_f32_r, (rocblas_int)d,
-                               rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
-          if (bs != rocblas_status_success) return fail(DPPO_ERR_HIP, "rocBLAS dweight GEMM failed (%d)", (int)bs);
-        }
+        if ((e = timed([&] { return dppo::launch_lmh_bwd_tiles(m, st); })) != hipSuccess)
+          return hip_fail(e, "backward tile launch");
+        s = products(n0, n1);
+        if (s != DPPO_OK) return s;
       }
     }
   }

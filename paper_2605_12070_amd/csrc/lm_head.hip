@@ -1,12 +1,16 @@
 // Loss stage with the LM head folded in (gfx950). The logits z = hidden weight^T exist only
 // as LMH_BM x LMH_BN tiles in registers and LDS:
-//   lmh_fwd_tiles  one tile per workgroup on the matrix cores, reduced to a per-token
-//                  partial log-sum-exp of the tile's LMH_BN vocabulary entries;
+//   lmh_fwd_tiles  one tile per workgroup on the matrix cores, reduced to per-token partial
+//                  log-sum-exps of each 128-entry vocabulary group; optionally also stores
+//                  the group-normalised exponentials 2^(z log2 e - m2) as fp16;
 //   lmh_zy         z[t, y_t] as one dot product per token;
-//   lmh_finish     merges the partials into lse_t and runs the token math of Eq. 1-4
-//                  (ratios, band, PPO clip, loss, MIS weight w_t);
-//   lmh_bwd_tiles  recomputes a tile and writes g = w_t (softmax - onehot) for one
-//                  vocabulary chunk, the operand of the two gradient products.
+//   lmh_grad_rows  per token row: merges the partials into lse_t, runs the token math of
+//                  Eq. 1-4 (ratios, band, PPO clip, loss, MIS weight w_t) and turns the
+//                  row's stored exponentials into G = w_t (softmax - onehot) in bf16, the
+//                  operand of the two gradient products (lm_head_grad.hip);
+//   lmh_finish     the same merge and token math without G (forward only, or the
+//                  vocabulary-chunk mode);
+//   lmh_bwd_tiles  vocabulary-chunk mode: recomputes a tile and writes G for one chunk.
 #include <type_traits>
 #include <utility>
 
@@ -59,8 +63,6 @@ constexpr int kAEl = LMH_BM * LMH_BK;           // bf16 elements of the A tile (
 constexpr int kStageEl = (LMH_BM + LMH_BN) * LMH_BK;
 static_assert(LMH_BK == 64 && LMH_BM % (kRL * kWaves) == 0 && LMH_BN % (kRL * kWaves) == 0,
               "tile shape");
-static_assert(LMH_WM * LMH_TM * LMH_WN * 32 * 8 <= LMH_STAGES * kStageEl * 2,
-              "the forward merge scratch fits in the ring");
 static_assert(LMH_STAGES >= 2 && (LMH_STAGES - 2) * (kIA + kIB) <= 63, "ring depth");
 static_assert((LMH_BK / 16) % 2 == 0, "an even number of K steps per stage");
 
@@ -243,20 +245,28 @@ struct LmhLane {
     lmh_engine(m, m0, r0, ring, epi);                                                     \
   } while (0)
 
-// Forward: per-token partial log-sum-exp (log2 domain) of one LMH_BN-entry vocabulary tile.
-// An entry of z that is NaN or +inf makes the partial sum NaN; a tile of only -inf logits
+// Forward: per-token partial log-sum-exp (log2 domain) of each 128-entry vocabulary group of
+// the tile (one wave's columns): m2 = log2 e * the group's maximum, sum 2^(z log2 e - m2).
+// With store_p the exponentials 2^(z log2 e - m2) in (0, 1] are also stored as fp16 into
+// g [T, ldg], four consecutive vocabulary entries (8 bytes) per store: the row pass later
+// scales them by w 2^(m2 - lse2) into the gradient, so the backward needs no second product.
+// ldg is then a multiple of the tile width, so every tile's columns lie inside the row
+// (entries past V are overwritten by the row pass); a buffer resource over the tile's token
+// rows drops the stores of rows past T.
+// An entry of z that is NaN or +inf makes the partial sum NaN; a group of only -inf logits
 // contributes nothing.
 __global__ __launch_bounds__(LMH_THREADS) void lmh_fwd_tiles(LmhArgs m) {
   const int m0 = blockIdx.x * LMH_BM;
   const int nt = blockIdx.y;
   const int r0 = m.n0 + nt * LMH_BN;
   const int ncols = min(LMH_BN, m.n1 - r0);
-  auto epi = [&](f32x16 (&acc)[LMH_TM][LMH_TN], float* scratch) {
+  auto epi = [&](f32x16 (&acc)[LMH_TM][LMH_TN], float*) {
     const LmhLane L;
-    // scratch[wm][mi][wn][token] of (n, s): the LMH_WN waves that share a token row merge
-    // through LDS
-    float2* xs = (float2*)scratch;
     const bool ragged = ncols < LMH_BN;       // only the last vocabulary tile
+    const int grp = (r0 / LMH_GROUP) + L.wn;  // this wave's 128 columns
+    const int prows = m.store_p ? min(LMH_BM, m.T - m0) : 0;
+    const __amdgpu_buffer_rsrc_t rp = row_rsrc(m.g + (int64_t)m0 * m.ldg, (int)(prows * m.ldg * 2));
+    static_assert(LMH_TN * 32 == LMH_GROUP, "a wave's columns form one group");
 #pragma unroll
     for (int mi = 0; mi < LMH_TM; ++mi) {
       float mx = -INFINITY;
@@ -267,35 +277,34 @@ __global__ __launch_bounds__(LMH_THREADS) void lmh_fwd_tiles(LmhArgs m) {
           const float x = acc[mi][ni][r];
           mx = fmaxf(mx, (ragged && L.vrow(ni, r) >= ncols) ? -INFINITY : x);
         }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));  // the two lanes that hold the token's group
       const float m2 = mx * kLog2e;
       const float sh = (mx == -INFINITY) ? 0.0f : m2;
+      const int t = L.token(m0, mi);
+      const int poff = (int)(((int64_t)(t - m0) * m.ldg + r0) * 2);
       float sum = 0.0f;
 #pragma unroll
       for (int ni = 0; ni < LMH_TN; ++ni)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = exp2_hw(__builtin_fmaf(acc[mi][ni][r], kLog2e, -sh));
-          sum += (ragged && L.vrow(ni, r) >= ncols) ? 0.0f : e;
-        }
-      float n = (mx == -INFINITY) ? -INFINITY : m2;
-      merge_ns(n, sum, __shfl_xor(n, 32, 64), __shfl_xor(sum, 32, 64));
-      if (L.lane < 32)
-        xs[((L.wm * LMH_TM + mi) * LMH_WN + L.wn) * 32 + L.lane] = make_float2(n, sum);
-    }
-    __syncthreads();
-    // one thread per token of the tile merges the LMH_WN partials
-    for (int i = threadIdx.x; i < LMH_BM; i += LMH_THREADS) {
-      const int wm = i / (32 * LMH_TM), mi = (i / 32) % LMH_TM, l = i % 32;
-      const int t = m0 + i;
-      float n = -INFINITY, sum = 0.0f;
+        for (int q = 0; q < 4; ++q) {
+          const int v0 = L.vrow(ni, 4 * q);
+          float e[4];
 #pragma unroll
-      for (int wn = 0; wn < LMH_WN; ++wn) {
-        const float2 v = xs[((wm * LMH_TM + mi) * LMH_WN + wn) * 32 + l];
-        merge_ns(n, sum, v.x, v.y);
-      }
-      if (t < m.T) {
-        float* p = m.part + ((int64_t)nt * m.T + t) * 2;
-        p[0] = n;
+          for (int j = 0; j < 4; ++j) {
+            e[j] = exp2_hw(__builtin_fmaf(acc[mi][ni][4 * q + j], kLog2e, -sh));
+            sum += (ragged && v0 + j >= ncols) ? 0.0f : e[j];
+          }
+          if (m.store_p) {
+            u32x2 v;
+            v.x = pack_f16(e[0], e[1]);
+            v.y = pack_f16(e[2], e[3]);
+            __builtin_amdgcn_raw_buffer_store_b64(v, rp, poff + v0 * 2, 0, 0);
+          }
+        }
+      sum += __shfl_xor(sum, 32, 64);
+      if (L.lane < 32 && t < m.T) {
+        float* p = m.part + ((int64_t)grp * m.T + t) * 2;
+        p[0] = (mx == -INFINITY) ? -INFINITY : m2;
         p[1] = sum;
       }
     }
@@ -350,9 +359,9 @@ __global__ __launch_bounds__(256) void lmh_finish(RowArgs a, LmhArgs m) {
       bad = true;
     } else {
       float n = -INFINITY, s = 0.0f;
-      const int ntiles = lmh_tiles(m.V);
+      const int ngroups = lmh_groups(m.V);
       const float* p = m.part + (int64_t)t * 2;
-      for (int i = 0; i < ntiles; ++i) merge_ns(n, s, p[(int64_t)i * m.T * 2], p[(int64_t)i * m.T * 2 + 1]);
+      for (int i = 0; i < ngroups; ++i) merge_ns(n, s, p[(int64_t)i * m.T * 2], p[(int64_t)i * m.T * 2 + 1]);
       l2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
       const TokenOut o = token_math(a, token_inputs_lane(a, t), m.zy[t], l2);
       a.lp_out[t] = o.lp;
@@ -381,8 +390,98 @@ __global__ __launch_bounds__(256) void lmh_finish(RowArgs a, LmhArgs m) {
   }
 }
 
-// Backward: g[t, v - n0] = w_t (softmax(z_t)[v] - 1{v = y_t}) in bf16 for the tile's rows
-// of the chunk [n0, n1); tokens that were not evaluated get zeros.
+// Full-vocabulary backward without a second product: one workgroup per token row, looping
+// over rows. Merges the row's group partials into lse2, runs the token math (per-token
+// outputs, counters kept per workgroup), then turns the row's stored exponentials into
+// G = w (softmax - onehot) in place: entry v of group q becomes w 2^(m2_q - lse2) e_v in
+// bf16, the sampled entry w (p_y - 1) as token_math computes it from z[y], and the entries
+// from V up to ldg become zeros. A row that is not evaluated (masked, or a bad id) becomes
+// zeros. Four 16-byte chunks per thread are in flight at a time.
+constexpr int kGR = 256;
+
+__global__ __launch_bounds__(kGR) void lmh_grad_rows(RowArgs a, LmhArgs m) {
+  __shared__ float red[2 * (kGR / 64) + 2];
+  __shared__ float bc[2];
+  StatCount sc;
+  const int tid = threadIdx.x;
+  const int ngroups = lmh_groups(m.V);
+  const int nchunk = (int)(m.ldg / 8);
+  for (int64_t row = blockIdx.x; row < m.T; row += gridDim.x) {
+    const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
+    const int64_t y = uload(m.ids + row);
+    const bool ev = valid && y >= 0 && y < m.V;           // uniform over the workgroup
+    float w = 0.0f, l2 = 0.0f, dy = 0.0f;
+    if (ev) {
+      float n = -INFINITY, s = 0.0f;
+      for (int q = tid; q < ngroups; q += kGR) {
+        const float* p = m.part + ((int64_t)q * m.T + row) * 2;
+        merge_ns(n, s, p[0], p[1]);
+      }
+      block_merge_ns<kGR>(n, s, red);
+      l2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+      if (tid == 0) {
+        const TokenOut o = token_math(a, token_inputs(a, row), uload(m.zy + row), l2);
+        a.lp_out[row] = o.lp;
+        a.loss_tok[row] = o.loss;
+        if (a.flags) a.flags[row] = o.flags;
+        count_stats(a, o.flags, sc);
+        bc[0] = o.w;
+        bc[1] = o.dy;
+      }
+      __syncthreads();
+      w = bc[0];
+      dy = bc[1];
+    } else if (tid == 0) {
+      a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
+      a.loss_tok[row] = 0.0f;
+      if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
+      if (valid) sc.bad += 1;
+    }
+    uint16_t* grow = m.g + row * m.ldg;
+    const float* prt = m.part + row * 2;
+    for (int c0 = tid; c0 < nchunk; c0 += 4 * kGR) {
+      u32x4 e[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = c0 + k * kGR;
+        e[k] = (ev && c < nchunk && 8 * c < m.V)
+                   ? __builtin_nontemporal_load((const u32x4*)(grow + 8 * c))
+                   : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = c0 + k * kGR;
+        if (c >= nchunk) break;
+        const int v0 = 8 * c;
+        u32x4 out = {0u, 0u, 0u, 0u};
+        if (ev && v0 < m.V) {
+          const float m2 = prt[(int64_t)(v0 / LMH_GROUP) * m.T * 2];
+          const float f = w * exp2_hw(m2 - l2);
+          float x[8];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            x[2 * j] = f16_lo_mul(e[k][j], f);
+            x[2 * j + 1] = f16_hi_mul(e[k][j], f);
+          }
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            if ((int64_t)(v0 + j) == y) x[j] = dy;
+            if (v0 + j >= m.V) x[j] = 0.0f;
+          }
+#pragma unroll
+          for (int j = 0; j < 4; ++j) out[j] = pack_bf16(x[2 * j], x[2 * j + 1]);
+        }
+        __builtin_nontemporal_store(out, (u32x4*)(grow + v0));
+      }
+    }
+  }
+  if (tid == 0) flush_stats(a, sc);
+}
+
+// Backward (vocabulary chunks): g[t, v - n0] = w_t (softmax(z_t)[v] - 1{v = y_t}) in bf16
+// for the tile's rows of the chunk [n0, n1); tokens that were not evaluated get zeros. The
+// last tile also zeroes the entries past the chunk up to the next multiple of 8, which the
+// gradient products read as whole 16-byte chunks.
 __global__ __launch_bounds__(LMH_THREADS) void lmh_bwd_tiles(LmhArgs m) {
   const int m0 = blockIdx.x * LMH_BM;
   const int r0 = m.n0 + blockIdx.y * LMH_BN;
@@ -416,7 +515,9 @@ __global__ __launch_bounds__(LMH_THREADS) void lmh_bwd_tiles(LmhArgs m) {
             v.y = pack_bf16(o[2], o[3]);
             *(u32x2*)(grow + v0) = v;
           } else {
-            for (int j = 0; j < 4 && v0 + j < ncols; ++j) grow[v0 + j] = to_bf16(o[j]);
+            const int end8 = (ncols + 7) & ~7;
+            for (int j = 0; j < 4 && v0 + j < end8; ++j)
+              grow[v0 + j] = v0 + j < ncols ? to_bf16(o[j]) : (uint16_t)0;
           }
         }
     }
@@ -437,6 +538,13 @@ hipError_t launch_lmh_fwd_tiles(const LmhArgs& m, hipStream_t st) {
 
 hipError_t launch_lmh_finish(const RowArgs& a, const LmhArgs& m, hipStream_t st) {
   lmh_finish<<<(m.T + 255) / 256, 256, 0, st>>>(a, m);
+  return hipGetLastError();
+}
+
+hipError_t launch_lmh_grad_rows(const RowArgs& a, const LmhArgs& m, hipStream_t st) {
+  if (m.ldg % 8 != 0) return hipErrorInvalidValue;
+  const int grid = m.T < 2048 ? m.T : 2048;
+  if (grid > 0) lmh_grad_rows<<<grid, kGR, 0, st>>>(a, m);
   return hipGetLastError();
 }
 
