@@ -238,6 +238,35 @@ dppo_status fused_lm_head_loss_fwd_bwd(
 int64_t fused_lm_head_workspace_bytes(int64_t T, int64_t d, int64_t V, int64_t vocab_chunk);
 
 /*
+ * fused_lm_head_loss_fwd_bwd_noalloc -- fused_lm_head_loss_fwd_bwd for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the workspace is the library's own static device scratch of
+ * fused_lm_head_noalloc_scratch_bytes() = 64 MiB, one copy on every device the library runs
+ * on, held until the process ends. The call allocates nothing (no hipMalloc, no allocating
+ * library routine); the caller still passes every input and output.
+ *  - It runs one pass (vocab_chunk 0) when that workspace fits the scratch, else the
+ *    largest chunk of 256-row multiples that fits; *vocab_chunk_used (host, nullable)
+ *    receives that value, and fused_lm_head_loss_fwd_bwd with the same vocab_chunk gives
+ *    the same bits. Sizes whose 256-row chunked workspace exceeds the scratch return
+ *    DPPO_ERR_UNSUPPORTED and enqueue nothing.
+ *  - Every call on a device shares that device's scratch, which keeps the last call's
+ *    contents (nothing in it needs clearing: every call writes what it reads). Calls that
+ *    overlap on one device (other streams, other host threads) race on it and must be
+ *    serialised by the caller.
+ * Every other argument and the error behaviour are those of fused_lm_head_loss_fwd_bwd.
+ */
+dppo_status fused_lm_head_loss_fwd_bwd_noalloc(
+    const void* hidden, const void* weight, int32_t dtype, int64_t T, int64_t d, int64_t V,
+    const int64_t* token_ids, const float* logp_mu_old, const float* logp_ref,
+    const float* advantages, const uint8_t* loss_mask, const float* token_scale,
+    const dppo_params* p, float* logp_out, float* loss_tok_out, float* loss_out,
+    uint8_t* flags_out, int32_t* stats_out, float* dhidden, float* dweight,
+    int64_t* vocab_chunk_used, void* stream);
+
+/* Bytes of the no-allocation variant's per-device scratch. */
+int64_t fused_lm_head_noalloc_scratch_bytes(void);
+
+/*
  * ewma_proxy_update -- one step of the PPO-EWMA reference (Sec. 5.2, Eq. 5; App. B) on a
  * flat buffer of n elements (proxy parameters, or per-token log-probs).
  *  normalized = 1: w_t = 1 + beta * w_{t-1};
@@ -422,7 +451,7 @@ const char* dppo_strerror(dppo_status s);
 const char* dppo_last_error(void);
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define DPPO_ABI_VERSION 5
+#define DPPO_ABI_VERSION 6
 int32_t dppo_abi_version(void);
 
 /*

@@ -25,6 +25,7 @@ __all__ = [
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
     "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
     "fused_lm_head_loss_fwd_bwd", "LmHeadResult", "lm_head_workspace_bytes",
+    "fused_lm_head_loss_fwd_bwd_noalloc",
     "logprob_fwd_versioned", "EwmaProxyDevice", "vocab_shard_stats", "vocab_shard_combine",
     "decoupled_ppo_loss_shard_fwd_bwd",
 ]
@@ -253,7 +254,7 @@ class LmHeadResult:
     stats: torch.Tensor         # [5] int32
     dhidden: torch.Tensor | None  # [T, d] fp32
     dweight: torch.Tensor | None  # [V, d] fp32
-    workspace: torch.Tensor     # scratch, reusable by the next call (out=)
+    workspace: torch.Tensor | None  # scratch, reusable by the next call (out=)
 
 
 def lm_head_workspace_bytes(T: int, d: int, V: int, vocab_chunk: int = 0) -> int:
@@ -313,6 +314,54 @@ def fused_lm_head_loss_fwd_bwd(hidden, weight, token_ids, logp_mu_old, logp_ref,
         int(vocab_chunk), out.workspace.data_ptr(), out.workspace.numel(), _stream(dev))
     _lib.check(st, "fused_lm_head_loss_fwd_bwd")
     return out
+
+
+def fused_lm_head_loss_fwd_bwd_noalloc(hidden, weight, token_ids, logp_mu_old, logp_ref,
+                                       advantages, loss_mask=None, token_scale=None, *,
+                                       band=(0.5, 2.0), clip_eps=(0.2, 0.2),
+                                       rd_mode="mask_weight", scale_mode="token_mean",
+                                       loss_scale=1.0, ref_mode="given", alpha=0.5,
+                                       want_grads=True, want_flags=True):
+    """fused_lm_head_loss_fwd_bwd with the library's static device scratch as workspace (the
+    C call allocates nothing). Returns (LmHeadResult, vocab_chunk_used); the result's
+    workspace field is None. Output tensors are allocated here, by the caller's side."""
+    for t, name in ((hidden, "hidden"), (weight, "weight")):
+        if t.dtype != torch.bfloat16 or t.dim() != 2 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"{name} must be a contiguous 2-D bf16 GPU tensor")
+    T, d = hidden.shape
+    V = weight.shape[0]
+    if weight.shape[1] != d:
+        raise ValueError("hidden and weight disagree on d")
+    dev = hidden.device
+    ids = _vec(token_ids, T, torch.int64, "token_ids", dev)
+    mu = _vec(logp_mu_old, T, torch.float32, "logp_mu_old", dev)
+    if ref_mode not in REF_MODES:
+        raise ValueError(f"ref_mode in {list(REF_MODES)}")
+    ref = _vec(logp_ref, T, torch.float32, "logp_ref", dev, optional=ref_mode != "given")
+    adv = _vec(advantages, T, torch.float32, "advantages", dev)
+    msk = _vec(loss_mask, T, torch.uint8, "loss_mask", dev, optional=True)
+    tsc = _vec(token_scale, T, torch.float32, "token_scale", dev, optional=True)
+    if rd_mode not in RD_MODES or scale_mode not in SCALE_MODES:
+        raise ValueError(f"rd_mode in {list(RD_MODES)}, scale_mode in {list(SCALE_MODES)}")
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = LmHeadResult(
+        loss=torch.empty(1, **f32), logp=torch.empty(T, **f32), loss_tok=torch.empty(T, **f32),
+        flags=torch.empty(T, dtype=torch.uint8, device=dev) if want_flags else None,
+        stats=torch.empty(_lib.N_STATS, dtype=torch.int32, device=dev),
+        dhidden=torch.empty(T, d, **f32) if want_grads else None,
+        dweight=torch.empty(V, d, **f32) if want_grads else None, workspace=None)
+    p = _lib.DppoParams(float(band[0]), float(band[1]), float(clip_eps[0]), float(clip_eps[1]),
+                        RD_MODES[rd_mode], SCALE_MODES[scale_mode], float(loss_scale),
+                        REF_MODES[ref_mode], float(alpha))
+    used = C.c_int64(-1)
+    st = _lib.lib().fused_lm_head_loss_fwd_bwd_noalloc(
+        hidden.data_ptr(), weight.data_ptr(), _lib.DTYPE_BF16, T, d, V, ids, mu, ref, adv, msk,
+        tsc, C.byref(p), out.logp.data_ptr(), out.loss_tok.data_ptr(), out.loss.data_ptr(),
+        out.flags.data_ptr() if out.flags is not None else None, out.stats.data_ptr(),
+        out.dhidden.data_ptr() if out.dhidden is not None else None,
+        out.dweight.data_ptr() if out.dweight is not None else None, C.byref(used), _stream(dev))
+    _lib.check(st, "fused_lm_head_loss_fwd_bwd_noalloc")
+    return out, used.value
 
 
 def ewma_proxy_update(x_prox: torch.Tensor, x_new: torch.Tensor, beta: float, w: float = 0.0,

@@ -21,7 +21,7 @@ STAT_N_VALID, STAT_N_BAND, STAT_N_PPO, STAT_N_ACTIVE, STAT_N_BAD = range(5)
 N_STATS = 5
 MAX_VERSIONS = 8
 DTYPE_F32, DTYPE_BF16 = 0, 1
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 # Every function the header declares, with its C signature.
 VP, I32, I64, F32, F64 = C.c_void_p, C.c_int32, C.c_int64, C.c_float, C.c_double
@@ -63,6 +63,10 @@ SIGNATURES = {
                                          C.POINTER(DppoParams), VP, VP, VP, VP, VP, VP, VP,
                                          I64, VP, I64, VP]),
     "fused_lm_head_workspace_bytes": (I64, [I64, I64, I64, I64]),
+    "fused_lm_head_loss_fwd_bwd_noalloc": (I32, [VP, VP, I32, I64, I64, I64, VP, VP, VP, VP, VP,
+                                                 VP, C.POINTER(DppoParams), VP, VP, VP, VP, VP,
+                                                 VP, VP, C.POINTER(I64), VP]),
+    "fused_lm_head_noalloc_scratch_bytes": (I64, []),
     "logprob_fwd_versioned": (I32, [C.POINTER(VP), I32, I32, I64, I64, I64, VP, VP, VP, VP, VP]),
     "dppo_effective_thresholds": (I32, [C.c_double, C.c_double, C.c_double, C.c_double,
                                         C.c_double, I32, C.POINTER(C.c_double)]),

@@ -624,6 +624,88 @@ dppo_status fused_lm_head_loss_fwd_bwd(
   return DPPO_OK;
 }
 
+}  // extern "C"
+
+// ------------------------------------------------------------------ no-allocation variant
+// Scratch of fused_lm_head_loss_fwd_bwd_noalloc: one copy on every device the library runs
+// on, held until the process ends. In host code `scratch` is only a stand-in for the
+// symbol; its device address comes from hipGetSymbolAddress, once per device.
+constexpr int64_t kNoallocScratchBytes = (int64_t)64 << 20;
+static __device__ __align__(256) char scratch[kNoallocScratchBytes];
+
+namespace {
+
+// Device address of `scratch` on the current device, looked up on the first call there.
+dppo_status scratch_address(void** out) {
+  static std::mutex mu;
+  static std::vector<std::pair<int, void*>> addr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lk(mu);
+  for (auto& kv : addr)
+    if (kv.first == dev) {
+      *out = kv.second;
+      return DPPO_OK;
+    }
+  void* p = nullptr;
+  e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  if (!p || ((uintptr_t)p & 255u)) return fail(DPPO_ERR_HIP, "scratch address %p not 256-byte aligned", p);
+  addr.push_back({dev, p});
+  *out = p;
+  return DPPO_OK;
+}
+
+// The vocab_chunk the no-allocation variant runs with: 0 (one pass) when its workspace fits
+// the scratch, else the largest multiple of 256 whose chunked workspace fits; -1 if none.
+int64_t noalloc_chunk(int64_t T, int64_t V) {
+  if (lmh_layout(T, V, 0).total <= kNoallocScratchBytes) return 0;
+  const int64_t vpad = ((V + dppo::LMH_BN - 1) / dppo::LMH_BN) * dppo::LMH_BN;
+  for (int64_t c = vpad - dppo::LMH_BN; c >= dppo::LMH_BN; ) {
+    const int64_t total = lmh_layout(T, V, c).total;
+    if (total <= kNoallocScratchBytes) return c;
+    // jump close to the largest chunk that fits, then step down by whole tiles
+    const int64_t over = (total - kNoallocScratchBytes + 2 * T - 1) / (2 * T);
+    c -= std::max<int64_t>(dppo::LMH_BN, (over + dppo::LMH_BN - 1) / dppo::LMH_BN * dppo::LMH_BN);
+  }
+  return -1;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t fused_lm_head_noalloc_scratch_bytes(void) { return kNoallocScratchBytes; }
+
+dppo_status fused_lm_head_loss_fwd_bwd_noalloc(
+    const void* hidden, const void* weight, int32_t dtype, int64_t T, int64_t d, int64_t V,
+    const int64_t* token_ids, const float* logp_mu_old, const float* logp_ref,
+    const float* advantages, const uint8_t* loss_mask, const float* token_scale,
+    const dppo_params* p, float* logp_out, float* loss_tok_out, float* loss_out,
+    uint8_t* flags_out, int32_t* stats_out, float* dhidden, float* dweight,
+    int64_t* vocab_chunk_used, void* stream) {
+  if (T < 0 || T >= ((int64_t)1 << 31) || V < 1 || V > ((int64_t)1 << 21))
+    return fail(DPPO_ERR_INVALID_ARG, "T = %lld or V = %lld out of range", (long long)T, (long long)V);
+  const int64_t chunk = T > 0 ? noalloc_chunk(T, V) : 0;
+  if (chunk < 0)
+    return fail(DPPO_ERR_UNSUPPORTED,
+                "T = %lld, V = %lld need more than the %lld-byte scratch of the no-allocation "
+                "variant even in 256-row vocabulary chunks; use fused_lm_head_loss_fwd_bwd with a "
+                "workspace", (long long)T, (long long)V, (long long)kNoallocScratchBytes);
+  void* ws = nullptr;
+  if (T > 0) {
+    const dppo_status s = scratch_address(&ws);
+    if (s != DPPO_OK) return s;
+  }
+  const dppo_status s = fused_lm_head_loss_fwd_bwd(
+      hidden, weight, dtype, T, d, V, token_ids, logp_mu_old, logp_ref, advantages, loss_mask,
+      token_scale, p, logp_out, loss_tok_out, loss_out, flags_out, stats_out, dhidden, dweight,
+      chunk, ws, T > 0 ? kNoallocScratchBytes : 0, stream);
+  if (s == DPPO_OK && vocab_chunk_used) *vocab_chunk_used = chunk;
+  return s;
+}
+
 dppo_status ewma_proxy_update(void* x_prox, const void* x_new, int32_t dtype, int64_t n,
                               float beta, double* w, int32_t reset, int32_t normalized,
                               void* stream) {

@@ -463,3 +463,19 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=300, cwd=root)
     assert p.returncode == 2, (p.returncode, p.stderr[-500:])
     assert "one GPU only" in p.stderr and p.stdout == ""
+
+
+def test_noalloc_rejects_sizes_beyond_its_scratch():
+    """Host-side checks of the no-allocation LM head: sizes whose 256-row chunked workspace
+    exceeds the static scratch are UNSUPPORTED, bad sizes INVALID_ARG, before any HIP call."""
+    L = _lib.lib()
+    p = _params()
+    used = C.c_int64(-7)
+    args = lambda T, V: (FAKE, FAKE, 1, T, 64, V, FAKE, FAKE, FAKE, FAKE, None, None, C.byref(p),
+                         FAKE, FAKE, FAKE, None, FAKE, None, None, C.byref(used), None)
+    assert L.fused_lm_head_loss_fwd_bwd_noalloc(*args(65536, 151936)) == _lib.DPPO_ERR_UNSUPPORTED
+    assert b"scratch" in L.dppo_last_error()
+    assert L.fused_lm_head_loss_fwd_bwd_noalloc(*args(-1, 100)) == _lib.DPPO_ERR_INVALID_ARG
+    assert L.fused_lm_head_loss_fwd_bwd_noalloc(*args(16, (1 << 21) + 1)) == _lib.DPPO_ERR_INVALID_ARG
+    assert used.value == -7
+
