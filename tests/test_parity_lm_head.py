@@ -143,15 +143,9 @@ def test_empty_batch():
     assert res.dweight.abs().sum().item() == 0.0
 
 
-def test_lm_head_workload_sampled_rows():
-    """The full-size LM-head workload (T = 8192, d = 4096, V = 151936): sampled rows of lp,
-    loss and dhidden against the oracle's row-level computation on z_t = hidden_t weight^T,
-    and the property that dweight's columns sum to zero over the vocabulary (each G row sums
-    to zero)."""
-    _say("lm_head full size")
+def _fullsize_inputs():
     wl = W.make_lm_head_workload(DEV)
-    T, V = wl.T, wl.V
-    z_rows = None
+    T = wl.T
     lp_anchor = torch.empty(T, dtype=torch.float64)
     # anchor from a float32 torch pass (input synthesis only)
     for a in range(0, T, 512):
@@ -160,23 +154,59 @@ def test_lm_head_workload_sampled_rows():
         lp_anchor[a:a + 512] = (z.gather(1, wl.ids[a:a + 512, None])[:, 0] - lse).double().cpu()
         del z
     lp_ref, lp_mu = W.reference_logprobs(lp_anchor, wl)
+    return wl, lp_ref, lp_mu
+
+
+def _z_rows(wl, rows, block=16384):
+    """Oracle logits z[rows] = hidden[rows] weight^T in float64 from the bf16 bits."""
+    H = bits_of(wl.hidden[torch.as_tensor(rows, device=DEV)])
+    V = wl.V
+    z = np.empty((len(rows), V))
+    for a in range(0, V, block):
+        z[:, a:a + block] = H @ bits_of(wl.weight[a:a + block]).T
+    return H, z
+
+
+def test_lm_head_workload_sampled_rows():
+    """The full-size LM-head workload (T = 8192, d = 4096, V = 151936, every token valid), as
+    the benchmark runs it: on 40 sampled rows (random, plus the first and the last), lp,
+    loss_tok and flags against the oracle's row-level computation on z_t = hidden_t weight^T,
+    and dhidden; on every row, the counters against the kernel's own flags; and dweight's
+    columns summing to zero over the vocabulary (each G row sums to zero)."""
+    _say("lm_head full size")
+    wl, lp_ref, lp_mu = _fullsize_inputs()
+    T, V = wl.T, wl.V
     res = P.fused_lm_head_loss_fwd_bwd(wl.hidden, wl.weight, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask)
     torch.cuda.synchronize()
-    rows = np.sort(np.random.default_rng(0).choice(T, size=6, replace=False))
-    Wt = bits_of(wl.weight)
-    H = bits_of(wl.hidden[torch.as_tensor(rows, device=DEV)])
-    z_rows = H @ Wt.T
+    rows = np.sort(np.concatenate([np.random.default_rng(0).choice(np.arange(1, T - 1), size=38,
+                                                                   replace=False), [0, T - 1]]))
+    H, z_rows = _z_rows(wl, rows)
     params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
     scale = oracle.batch_scale(wl.mask.cpu().numpy(), params)
     ref = oracle.per_token(z_rows, wl.ids.cpu().numpy()[rows], lp_mu.cpu().double().numpy()[rows],
                            lp_ref.cpu().double().numpy()[rows], wl.adv.cpu().double().numpy()[rows],
                            wl.mask.cpu().numpy()[rows], None, params, scale, want_dlogits=True)
+    ties = tie_mask(ref, params)
     lp = res.logp.cpu().double().numpy()[rows]
     assert_close_rel(lp, ref["lp"], 1e-4, "lp")
-    dh_ref = ref["dlogits"] @ Wt
+    lt = res.loss_tok.cpu().double().numpy()[rows]
+    assert_close_rel(lt, ref["loss_tok"], 1e-4, "loss_tok", mask=~ties)
+    fl_all = res.flags.cpu().numpy()
+    assert np.array_equal(fl_all[rows][~ties], ref["flags"][~ties]), "flags differ away from ties"
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl_all, params))
+    assert st[0] == T
     dh = res.dhidden[torch.as_tensor(rows, device=DEV)].cpu().double().numpy()
-    bound = _grad_bound(ref["dlogits"], Wt)
-    assert np.all(np.abs(dh - dh_ref) <= bound)
+    G = ref["dlogits"].copy()
+    G[ties] = 0.0
+    dh_ref = np.zeros_like(dh)
+    bound = np.zeros_like(dh)
+    for a in range(0, V, 16384):
+        Wb = bits_of(wl.weight[a:a + 16384])
+        dh_ref += G[:, a:a + 16384] @ Wb
+        bound += 2.0 ** -7 * (np.abs(G[:, a:a + 16384]) @ np.abs(Wb))
+    keep = ~ties
+    assert np.all(np.abs(dh - dh_ref)[keep] <= bound[keep] + 1e-7)
     # sum_v dweight[v] = sum_t (sum_v G[t, v]) hidden_t and every G row sums to zero; the
     # bf16 rounding of G leaves at most 2^-8 sum_v |G[t, v]| <= 2^-8 * 2 |w_t| per row, with
     # |w_t| <= s wd r_s |A| <= (1 / n_valid) * 2 * 1.2 * 1 here (band [0.5, 2], clip 0.2)
@@ -184,4 +214,68 @@ def test_lm_head_workload_sampled_rows():
     n_valid = int(wl.mask.sum().item())
     habs = wl.hidden.float().abs().double().sum(dim=0).cpu().numpy()
     assert np.all(np.abs(col) <= 2.0 ** -7 * (4.8 / n_valid) * habs + 1e-9)
-    _say("lm_head full size ok", res.stats.cpu().numpy().tolist())
+    _say("lm_head full size ok", st.tolist(), "ties", int(ties.sum()))
+
+
+@pytest.mark.parametrize("vocab_chunk", [0, 38000])
+def test_lm_head_fullsize_few_valid_tokens_every_gradient_entry(vocab_chunk):
+    """The full-size launch (T = 8192, d = 4096, V = 151936: every tile of every kernel runs)
+    with only 64 valid tokens, so that the oracle can form the whole gradient: every entry of
+    dweight (all 151936 rows, including the last ragged vocabulary tile and the rows of the
+    sampled ids) and of dhidden, plus the per-token outputs and the counters. The 64 valid
+    tokens are drawn from candidates whose ratios lie away from every threshold, so no
+    decision is a tie. vocab_chunk 38000 (rounded to 38144: four chunks, the last ragged)
+    runs the chunked backward at this size; 0 runs the one-pass backward."""
+    _say("lm_head full size, 64 valid tokens", vocab_chunk)
+    wl, lp_ref, lp_mu = _fullsize_inputs()
+    T, V = wl.T, wl.V
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    cand = np.sort(np.random.default_rng(5).choice(T, size=96, replace=False))
+    H_c, z_c = _z_rows(wl, cand)
+    probe = oracle.per_token(z_c, wl.ids.cpu().numpy()[cand], lp_mu.cpu().double().numpy()[cand],
+                             lp_ref.cpu().double().numpy()[cand], wl.adv.cpu().double().numpy()[cand],
+                             np.ones(len(cand), np.uint8), None, params, 1.0, want_dlogits=False)
+    ok = np.nonzero(~tie_mask(probe, params))[0][:64]
+    assert ok.size == 64
+    rows = cand[ok]
+    mask = torch.zeros(T, dtype=torch.uint8, device=DEV)
+    mask[torch.as_tensor(rows, device=DEV)] = 1
+    res = P.fused_lm_head_loss_fwd_bwd(wl.hidden, wl.weight, wl.ids, lp_mu, lp_ref, wl.adv, mask,
+                                       vocab_chunk=vocab_chunk)
+    torch.cuda.synchronize()
+    H, z = H_c[ok], z_c[ok]
+    m_np = mask.cpu().numpy()
+    scale = oracle.batch_scale(m_np, params)
+    ref = oracle.per_token(z, wl.ids.cpu().numpy()[rows], lp_mu.cpu().double().numpy()[rows],
+                           lp_ref.cpu().double().numpy()[rows], wl.adv.cpu().double().numpy()[rows],
+                           m_np[rows], None, params, scale, want_dlogits=True)
+    assert not tie_mask(ref, params).any()
+    lp = res.logp.cpu().double().numpy()
+    assert_close_rel(lp[rows], ref["lp"], 1e-4, "lp")
+    assert np.all(lp[m_np == 0] == 0.0)
+    assert_close_rel(res.loss_tok.cpu().double().numpy()[rows], ref["loss_tok"], 1e-4, "loss_tok")
+    fl = res.flags.cpu().numpy()
+    assert np.array_equal(fl[rows], ref["flags"]) and np.all(fl[m_np == 0] == 0)
+    np.testing.assert_array_equal(res.stats.cpu().numpy(), ref["stats"] if "stats" in ref
+                                  else oracle.stats_of(ref["flags"], params))
+    G = ref["dlogits"]
+    dh = res.dhidden.cpu().double().numpy()
+    assert np.all(dh[m_np == 0] == 0.0)
+    dh_ref = np.zeros((64, H.shape[1]))
+    dh_bound = np.zeros_like(dh_ref)
+    dw = res.dweight
+    worst = 0.0
+    for a in range(0, V, 16384):
+        b = min(V, a + 16384)
+        Wb = bits_of(wl.weight[a:b])
+        Gb = G[:, a:b]
+        dh_ref += Gb @ Wb
+        dh_bound += 2.0 ** -7 * (np.abs(Gb) @ np.abs(Wb))
+        dw_ref = Gb.T @ H
+        dw_bound = 2.0 ** -7 * (np.abs(Gb).T @ np.abs(H)) + 1e-7
+        err = np.abs(dw[a:b].cpu().double().numpy() - dw_ref)
+        assert np.all(err <= dw_bound), f"dweight rows {a}..{b}: worst excess {np.max(err - dw_bound):.3e}"
+        worst = max(worst, float(np.max(err / dw_bound)))
+    err = np.abs(dh[rows] - dh_ref)
+    assert np.all(err <= dh_bound + 1e-7), f"dhidden: worst excess {np.max(err - dh_bound - 1e-7):.3e}"
+    _say("lm_head 64 valid ok", vocab_chunk, "worst dW err / bound", round(worst, 4))
