@@ -29,8 +29,9 @@ struct LmhArgs {
   const uint16_t* weight;  // [V, d] bf16 (LM head, [out, in] layout)
   int32_t T, d, V;
   int32_t n0, n1;          // vocabulary rows [n0, n1) covered by a launch
-  float* part;             // forward: (m2, sum 2^(z log2 e - m2)) per (group, token), with
-                           // m2 = log2 e * the group's maximum; [groups][T] float pairs
+  float* part;             // forward: (m2, sum 2^(z log2 e - m2)) per (token, group), with
+                           // m2 = log2 e * the group's maximum; [T][groups] float pairs, so a
+                           // token's partials are contiguous for the row pass
   float* zy;               // z[t, y_t] (dot-product kernel)
   float* w;                // MIS weight per token (0 where the gradient is zero)
   float* lse2;             // log2 sum_v 2^(z log2 e) per token

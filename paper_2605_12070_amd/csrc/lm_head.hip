@@ -303,7 +303,7 @@ __global__ __launch_bounds__(LMH_THREADS) void lmh_fwd_tiles(LmhArgs m) {
         }
       sum += __shfl_xor(sum, 32, 64);
       if (L.lane < 32 && t < m.T) {
-        float* p = m.part + ((int64_t)grp * m.T + t) * 2;
+        float* p = m.part + ((int64_t)t * lmh_groups(m.V) + grp) * 2;
         p[0] = (mx == -INFINITY) ? -INFINITY : m2;
         p[1] = sum;
       }
@@ -360,8 +360,8 @@ __global__ __launch_bounds__(256) void lmh_finish(RowArgs a, LmhArgs m) {
     } else {
       float n = -INFINITY, s = 0.0f;
       const int ngroups = lmh_groups(m.V);
-      const float* p = m.part + (int64_t)t * 2;
-      for (int i = 0; i < ngroups; ++i) merge_ns(n, s, p[(int64_t)i * m.T * 2], p[(int64_t)i * m.T * 2 + 1]);
+      const float* p = m.part + (int64_t)t * ngroups * 2;
+      for (int i = 0; i < ngroups; ++i) merge_ns(n, s, p[2 * i], p[2 * i + 1]);
       l2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
       const TokenOut o = token_math(a, token_inputs_lane(a, t), m.zy[t], l2);
       a.lp_out[t] = o.lp;
@@ -414,7 +414,7 @@ __global__ __launch_bounds__(kGR) void lmh_grad_rows(RowArgs a, LmhArgs m) {
     if (ev) {
       float n = -INFINITY, s = 0.0f;
       for (int q = tid; q < ngroups; q += kGR) {
-        const float* p = m.part + ((int64_t)q * m.T + row) * 2;
+        const float* p = m.part + (row * ngroups + q) * 2;
         merge_ns(n, s, p[0], p[1]);
       }
       block_merge_ns<kGR>(n, s, red);
@@ -438,7 +438,7 @@ __global__ __launch_bounds__(kGR) void lmh_grad_rows(RowArgs a, LmhArgs m) {
       if (valid) sc.bad += 1;
     }
     uint16_t* grow = m.g + row * m.ldg;
-    const float* prt = m.part + row * 2;
+    const float* prt = m.part + row * ngroups * 2;
     for (int c0 = tid; c0 < nchunk; c0 += 4 * kGR) {
       u32x4 e[4];
 #pragma unroll
@@ -455,7 +455,7 @@ __global__ __launch_bounds__(kGR) void lmh_grad_rows(RowArgs a, LmhArgs m) {
         const int v0 = 8 * c;
         u32x4 out = {0u, 0u, 0u, 0u};
         if (ev && v0 < m.V) {
-          const float m2 = prt[(int64_t)(v0 / LMH_GROUP) * m.T * 2];
+          const float m2 = prt[(v0 / LMH_GROUP) * 2];
           const float f = w * exp2_hw(m2 - l2);
           float x[8];
 #pragma unroll

@@ -12,14 +12,17 @@
 //
 // Tile engine: 4 waves (2 x 2, one per SIMD), each with 4 x 4 tiles of
 // v_mfma_f32_32x32x16_bf16, so a workgroup covers 256 x 256 of C and a wave 128 x 128 (256
-// accumulation registers). K advances 64 per LDS stage; two stages of 64 KB form a ring,
-// filled by 16-byte buffer-to-LDS loads (lane l's 16 bytes land at the wave's LDS base +
-// 16 l; a lane whose offset lies outside the buffer resource receives zeros, which bounds
-// every access to the matrix and turns every tail into zeros).
-//  * A K-major operand tile is 256 staged rows of 64 K (128 bytes); its 16-byte chunk c of
-//    row r sits at position c ^ ((r / 2) % 8). A fragment (one lane: 8 consecutive K of one
-//    row) is one 16-byte LDS read, and 16 lanes cover all 64 banks.
-//  * An MN-major operand tile is 64 staged rows of K, each 256 M (or N) entries (512
+// accumulation registers). K advances GBK = 32 per LDS stage; four stages of 32 KB form a
+// ring (each slot its own LDS object), filled by 16-byte buffer-to-LDS loads (lane l's 16
+// bytes land at the wave's LDS base + 16 l; a lane whose offset lies outside the buffer
+// resource receives zeros, which bounds every access to the matrix and turns every tail into
+// zeros). A slot is refilled three stages ahead of its use: on MI355X four 32-deep stages
+// ran 3 % faster than two 64-deep ones, and five (the whole 160 KB of LDS) no faster.
+//  * A K-major operand tile is 256 staged rows of GBK K (GBK / 8 16-byte chunks); chunk c of
+//    row r sits at position c ^ sw_k(r), so the 16 consecutive rows of one fragment read
+//    pass cover all 64 banks. A fragment (one lane: 8 consecutive K of one row) is one
+//    16-byte LDS read.
+//  * An MN-major operand tile is GBK staged rows of K, each 256 M (or N) entries (512
 //    bytes); chunk c of row r sits at position c ^ (4 (r % 4)). A fragment is read with two
 //    transposing LDS reads (ds_read_b64_tr_b16): within each 16-lane block, lane s reads 4
 //    consecutive entries of row k0 + s / 4 at column c0 + 4 (s % 4), and lane i receives
@@ -55,16 +58,25 @@ constexpr int GW_M = 2, GW_N = 2;                // waves
 constexpr int GTM = 4, GTN = 4;                  // 32 x 32 tiles per wave
 constexpr int GBM = 32 * GW_M * GTM;             // 256
 constexpr int GBN = 32 * GW_N * GTN;             // 256
-constexpr int GBK = 64;
+#ifndef LMG_BK
+#define LMG_BK 32
+#endif
+#ifndef LMG_STAGES
+#define LMG_STAGES 4
+#endif
+constexpr int GBK = LMG_BK;                      // K per LDS stage
 constexpr int GTHREADS = 64 * GW_M * GW_N;
-constexpr int GS = 2;                            // LDS stages
-constexpr int kOpEl = 256 * 64;                  // bf16 elements of one operand tile
+constexpr int GS = LMG_STAGES;                   // LDS stages
+constexpr int kOpEl = 256 * GBK;                 // bf16 elements of one operand tile
 constexpr int kLoads = kOpEl * 2 / 1024 / (GW_M * GW_N);  // wave loads per operand, stage
-static_assert(GBM == LMH_GBM && GBN == LMH_GBN && GBK == 64 && kLoads == 8, "tile shape");
+constexpr int kC = GBK / 8;                      // 16-byte chunks per K-major staged row
+constexpr int kRL = 64 / kC;                     // K-major rows per wave load
+static_assert(GBM == LMH_GBM && GBN == LMH_GBN && (GBK == 64 || GBK == 32), "tile shape");
 
 template <int N> using IC = std::integral_constant<int, N>;
 
-__device__ __forceinline__ int sw_k(int r) { return (r >> 1) & 7; }   // K-major rows
+// K-major rows: 16 consecutive rows (one 16-lane read pass) land on 16 distinct bank groups
+__device__ __forceinline__ int sw_k(int r) { return (r / (16 / kC)) % kC; }
 __device__ __forceinline__ int sw_mn(int r) { return (r & 3) << 2; }  // MN-major rows
 
 constexpr int kOob = 0x7fffff00;  // an offset past every resource: the load returns zeros
@@ -89,13 +101,13 @@ struct Operand {
     o0 = o0_;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     if constexpr (!MN) {
-      // load i: tile rows 8 (wave kLoads + i) .. +7; lane -> row l / 8, position l % 8
+      // load i: tile rows kRL (wave kLoads + i) .. +kRL-1; lane -> row l / kC, position l % kC
       const int rows = min(256, ext - o0);
       rs = row_rsrc(p + (int64_t)o0 * ld, rows > 0 ? (int)(rows * ld * 2) : 0);
 #pragma unroll
       for (int i = 0; i < kLoads; ++i) {
-        const int row = 8 * (wave * kLoads + i) + (lane >> 3);
-        off[i] = (int)(row * ld * 2) + (((lane & 7) ^ sw_k(row)) * 16);
+        const int row = kRL * (wave * kLoads + i) + lane / kC;
+        off[i] = (int)(row * ld * 2) + (((lane % kC) ^ sw_k(row)) * 16);
       }
     } else {
       // load i: staged rows (K) 2 (wave kLoads + i), +1; lane -> row l / 32, position l % 32
@@ -130,8 +142,8 @@ struct Operand {
     int o;
     if constexpr (!MN) {
       const int k0 = kb * GBK;
-      const int row = 8 * (wave * kLoads + I) + (lane >> 3);
-      const int kc = (lane & 7) ^ sw_k(row);
+      const int row = kRL * (wave * kLoads + I) + lane / kC;
+      const int kc = (lane % kC) ^ sw_k(row);
       o = (k0 + kc * 8 < K) ? off[I] + k0 * 2 : kOob;
     } else {
       o = off[I];
@@ -153,7 +165,7 @@ struct Frags {
     if constexpr (!MN) {
       const int row = wo + (lane & 31);
 #pragma unroll
-      for (int f = 0; f < 4; ++f) base[f] = (row + 32 * f) * 128;
+      for (int f = 0; f < 4; ++f) base[f] = (row + 32 * f) * GBK * 2;
     } else {
       const int b = lane >> 4, s = lane & 15, q = s >> 2, e = s & 3;
 #pragma unroll
@@ -329,9 +341,19 @@ __device__ __forceinline__ int xcd_tile(int i, int nt) {
 // C (+)= A B^T over the tile of workgroup blockIdx.x; fp32 C stored non-temporally.
 template <bool AMN, bool BMN>
 __global__ __launch_bounds__(GTHREADS) void lmh_grad_gemm(GemmArgs g) {
-  static_assert(GS == 2, "two LDS slots");
-  __shared__ __align__(16) uint16_t la0[kOpEl], lb0[kOpEl], la1[kOpEl], lb1[kOpEl];
-  const Ring ring{{la0, la1}, {lb0, lb1}};
+  // one LDS object per slot and operand (a 2-D array is one object: the transposing reads of
+  // one slot would then wait for the loads into another); unused ones are not allocated
+  static_assert(GS >= 2 && GS <= 5, "LDS slots");
+  __shared__ __align__(16) uint16_t la0[kOpEl], la1[kOpEl], la2[kOpEl], la3[kOpEl], la4[kOpEl];
+  __shared__ __align__(16) uint16_t lb0[kOpEl], lb1[kOpEl], lb2[kOpEl], lb3[kOpEl], lb4[kOpEl];
+  uint16_t* const as[5] = {la0, la1, la2, la3, la4};
+  uint16_t* const bs[5] = {lb0, lb1, lb2, lb3, lb4};
+  Ring ring;
+#pragma unroll
+  for (int i = 0; i < GS; ++i) {
+    ring.a[i] = as[i];
+    ring.b[i] = bs[i];
+  }
   const int L = xcd_tile(blockIdx.x, g.tiles_m * g.tiles_n);
   const int m0 = (L / g.tiles_n) * GBM;
   const int n0 = (L % g.tiles_n) * GBN;
