@@ -257,6 +257,49 @@ def vocab_shard_measure(dev, wl, lp_mu, lp_ref, n_shards=8, reps=20):
             "tokens_per_s": round(T / ((c_stats + c_loss) * 1e-3), 1)}
 
 
+def fp32_rows_measure(dev, T=8192, V=151936, reps=10):
+    """fp32 logits with rows longer than the register-resident kernels hold: T = 8192,
+    V = 151936 (N(0, 3^2), uniform token ids, every token valid), the fused forward and
+    backward. Timed by the library's events around the per-row kernel (the resident-prefix
+    kernel); algorithmic bytes as for the bf16 rows (logits read once, dlogits written
+    once, 29 B of per-token vectors)."""
+    g = torch.Generator(device=dev).manual_seed(7)
+    z = torch.empty(T, V, dtype=torch.float32, device=dev)
+    for a in range(0, T, 1024):
+        z[a:a + 1024] = 3.0 * torch.randn(min(1024, T - a), V, generator=g, device=dev)
+    ids = torch.randint(0, V, (T,), generator=g, device=dev)
+    anchor = anchor_logprob(z, ids)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=dev, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.05 * torch.randn(T, generator=g, device=dev,
+                                                  dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=dev)
+    dl = torch.empty_like(z)
+    out = None
+    for _ in range(3):
+        out = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, dlogits=dl, out=out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with P.KernelTimer() as kt:
+        e0.record(stream)
+        for _ in range(reps):
+            out = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, dlogits=dl, out=out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        k_ms, k_n = kt.read()
+    call_ms = e0.elapsed_time(e1) / reps
+    ms = k_ms / max(1, k_n)
+    b_alg = algorithmic_bytes(T, V, T, 4, 29)
+    gbps = b_alg / (ms * 1e-3) / 1e9
+    del z, dl, out
+    return {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(gbps / HBM_PEAK_GBPS, 4),
+            "kernel": P.row_kernel_name(torch.float32, V), "kernel_ms": round(ms, 4),
+            "alg_bytes_per_launch": b_alg, "workload": f"fp32 rows T={T} V={V}",
+            "call_ms": round(call_ms, 4), "tokens_per_s": round(T / (call_ms * 1e-3), 1),
+            "traffic": recorded_traffic("fp32_rows")}
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, AMD specification
 
 
@@ -374,6 +417,8 @@ def main():
                     help="skip the vocabulary-shard measurement")
     ap.add_argument("--no-versioned", action="store_true",
                     help="skip the versioned log-prob measurement")
+    ap.add_argument("--no-fp32", action="store_true",
+                    help="skip the fp32 long-row measurement")
     ap.add_argument("--flush-mb", type=int, default=-1,
                     help="write this many MB before every timed step and report medians "
                          "(default: 512 for tiny and small_vocab, whose working set fits the "
@@ -463,6 +508,9 @@ def main():
         if args.workload == "large_vocab":
             vr["traffic"] = recorded_traffic("versioned_logprob")
         result["versioned_logprob_roofline"] = vr
+    if not args.no_fp32 and args.workload == "large_vocab":
+        log("fp32 long rows")
+        result["fp32_rows_roofline"] = fp32_rows_measure(dev)
     if args.ewma_elems > 0:
         result["ewma_roofline"] = ewma_bandwidth(dev, args.ewma_elems)
     if not args.no_lm_head:

@@ -264,7 +264,9 @@ const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t w
   thread_local char buf[96];
   const char* ty = dtype == DPPO_BF16 ? "bf16" : "f32";
   const char* bw = with_dlogits ? "true" : "false";
-  if (L.resident && dtype == DPPO_BF16 && !with_dlogits)
+  if (L.prefix)
+    snprintf(buf, sizeof(buf), "dppo::rows_f32_prefix<%d, %d>", L.threads, L.chunks);
+  else if (L.resident && dtype == DPPO_BF16 && !with_dlogits)
     snprintf(buf, sizeof(buf), "dppo::rows_bf16_fwd<%d, %d>", L.threads, L.chunks);
   else if (L.two_buffers)
     snprintf(buf, sizeof(buf), "dppo::rows_bf16_resident_db<%d, %d>", L.threads, L.chunks);

@@ -726,6 +726,173 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgsOf<BWD> a) {
 }
 
 // ---------------------------------------------------------------------------------------
+// fp32 rows with dlogits that are longer than the register-resident kernels hold
+// (V > 4 NT NC): the first NT x NC 16-byte chunks of a row stay in registers between the
+// two passes, exponentials written back in place as in rows_f32_resident, and only the rest
+// of the row (the tail) is read a second time. Per row: V elements read, V - 4 NT NC read
+// again, V written, against 2 V read and V written by the streaming kernel. Persistent, one
+// workgroup per row at a time.
+// Pass A streams the tail four chunks per thread at a time (chunks NT NC + tid, + NT, ...;
+// the last may be partial) and merges each as a general (max, sum) partial, then loads the
+// resident chunks and gives them one shift per thread, as the resident kernel does. Pass B
+// scales the resident exponentials into dlogits, then re-reads the tail. Element e of the row is read and written by the same thread, so dlogits may alias
+// the logits.
+// ---------------------------------------------------------------------------------------
+template <int NT>
+__device__ void skip_row_long(const RowArgs& a, int64_t row, bool valid, StatCount& sc) {
+  using C = Chunk<float, true>;
+  if (a.dlogits) {
+    float* d = (float*)a.dlogits + row * a.ldd;
+    const int nchunk = (a.V + 3) >> 2;
+    const float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int idx = threadIdx.x; idx < nchunk; idx += NT) C::store(d, idx, a.V, z);
+  }
+  if (threadIdx.x == 0) {
+    a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
+    a.loss_tok[row] = 0.0f;
+    if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
+    if (valid) sc.bad += 1;
+  }
+}
+
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
+  constexpr int P = NT * NC;              // resident chunks of a row
+  constexpr int U = 4;                    // tail chunks per thread in flight
+  __shared__ float red[2 * (NT / 64) + 2];
+  __shared__ Bcast bc;
+  StatCount sc;
+  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
+    const int tid = threadIdx.x;
+    const int V = a.V;
+    const int nfull = V >> 2;             // whole 16-byte chunks, > P by the selection
+    const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
+    const int64_t y = uload(a.ids + row);
+    const bool good = (y >= 0) && (y < V);
+    if (!(valid && good)) {               // uniform
+      skip_row_long<NT>(a, row, valid, sc);
+      continue;
+    }
+    const float* zrow = (const float*)a.logits + row * a.ld;
+    float zy = 0.0f;
+    if (tid == 0) zy = zrow[y];
+    // Whole chunks through a resource over the row: a chunk past the end (offset kOff)
+    // loads zeros, replaced by -inf below. The V % 4 last elements belong to one thread.
+    const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, nfull * 16);
+    constexpr int kOff = 0x7fffff00;
+    const bool rag_owner = (V & 3) != 0 && tid == nfull % NT;
+    // pass A, tail first, so that its registers and the resident chunks are never live
+    // together
+    float nt = -INFINITY, st = 0.0f;
+    for (int i0 = P + tid; i0 < nfull; i0 += U * NT) {
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = i0 + u * NT;
+        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool in = i0 + u * NT < nfull;
+        float x[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = in ? __uint_as_float(v[u][j]) : -INFINITY;
+        const float m = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+        const float ns = (m == -INFINITY) ? 0.0f : m * kLog2e;
+        float cs = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cs += exp2_hw(__builtin_fmaf(x[j], kLog2e, -ns));
+        merge_ns(nt, st, (m == -INFINITY) ? -INFINITY : ns, cs);
+      }
+    }
+    if (rag_owner) {
+      for (int e = nfull * 4; e < V; ++e) {
+        const float x = zrow[e];
+        const float ns = (x == -INFINITY) ? 0.0f : x * kLog2e;
+        merge_ns(nt, st, (x == -INFINITY) ? -INFINITY : ns, exp2_hw(__builtin_fmaf(x, kLog2e, -ns)));
+      }
+    }
+    // pass A, resident chunks: one shift per thread, exponentials in place
+    float r[NC][4];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const u32x4 v = buf_load16(rz, tid * 16, c * NT * 16);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r[c][j] = __uint_as_float(v[j]);
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      m = max3(m, r[c][0], r[c][1]);
+      m = max3(m, r[c][2], r[c][3]);
+    }
+    const float n_shift = (m == -INFINITY) ? 0.0f : m * kLog2e;
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) r[c][j] = exp2_hw(__builtin_fmaf(r[c][j], kLog2e, -n_shift));
+      s0 += r[c][0]; s1 += r[c][1]; s2 += r[c][2]; s3 += r[c][3];
+    }
+    const float n_mine = (m == -INFINITY) ? -INFINITY : n_shift;
+    float n = n_mine;
+    float s = (s0 + s1) + (s2 + s3);
+    merge_ns(n, s, nt, st);
+    block_merge_ns<NT>(n, s, red);
+    const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    if (!a.dlogits) continue;             // uniform
+    __syncthreads();
+    const float w = bc.w;
+    const float dy = bc.dy;
+    const float l2 = bc.lse2;
+    const float f = row_factor(w, n_mine, l2);
+    float* drow = (float*)a.dlogits + row * a.ldd;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
+    // pass B, resident chunks (the sampled entry: the thread that holds it)
+    const int cy = (int)(y >> 2);
+    const int jy = (int)(y & 3);
+    const int my_slot = (cy < P && cy % NT == tid) ? cy / NT : -1;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      float o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[j] = (c == my_slot && j == jy) ? dy : r[c][j] * f;
+      const u32x4 v = {__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                       __float_as_uint(o[3])};
+      buf_store16_nt(v, rd, tid * 16, c * NT * 16);
+    }
+    // pass B, tail: re-read, scale, store (stores past the row are dropped)
+    for (int i0 = P + tid; i0 < nfull; i0 += U * NT) {
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = i0 + u * NT;
+        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = i0 + u * NT;
+        float o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          o[j] = w * exp2_hw(__builtin_fmaf(__uint_as_float(v[u][j]), kLog2e, -l2));
+          o[j] = (idx == cy && j == jy) ? dy : o[j];
+        }
+        const u32x4 ov = {__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                          __float_as_uint(o[3])};
+        buf_store16_nt(ov, rd, idx < nfull ? idx * 16 : kOff, 0);
+      }
+    }
+    if (rag_owner) {
+      for (int e = nfull * 4; e < V; ++e)
+        drow[e] = (e == y) ? dy : w * exp2_hw(__builtin_fmaf(zrow[e], kLog2e, -l2));
+    }
+  }
+  if (threadIdx.x == 0) flush_stats(a, sc);
+}
+
+// ---------------------------------------------------------------------------------------
 // Valid-token count (prepares stats for the token-mean scale) and the loss sum.
 // ---------------------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void prep_stats(const uint8_t* mask, int64_t T, int32_t* stats) {
@@ -903,6 +1070,16 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   }
   L.threads = 1024;
   L.resident = false;
+  if (dtype == DPPO_F32 && bwd && aligned && force != kForceStream &&
+      V / 4 >= (int64_t)1024 * kPrefixNC) {
+    // longer fp32 rows: a resident prefix of 1024 x kPrefixNC whole chunks, the rest (and a
+    // ragged end) streamed twice
+    L.fn = (const void*)rows_f32_prefix<1024, kPrefixNC>;
+    L.chunks = kPrefixNC;
+    L.prefix = true;
+    L.persistent = true;
+    return L;
+  }
   if (dtype == DPPO_BF16) {
     L.fn = aligned ? (bwd ? (const void*)rows_stream<uint16_t, 1024, true, true>
                           : (const void*)rows_stream<uint16_t, 1024, false, true>)

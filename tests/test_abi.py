@@ -317,6 +317,13 @@ def test_row_kernel_name_follows_the_selection_rule():
     assert row_kernel_name(bf, 77825).startswith("dppo::rows_stream")      # ragged chunk
     assert row_kernel_name(bf, 64, ld=68).endswith("true, false>")          # unaligned stride
     assert row_kernel_name(f32, 32000) == "dppo::rows_f32_resident<1024, 8, true>"
+    # fp32 rows past the resident kernels: a resident prefix and a streamed tail when the
+    # row holds at least the prefix's 1024 x 19 whole chunks; otherwise the streaming kernel
+    assert row_kernel_name(f32, 151936) == "dppo::rows_f32_prefix<1024, 19>"
+    assert row_kernel_name(f32, 77825, ld=77828) == "dppo::rows_f32_prefix<1024, 19>"
+    assert row_kernel_name(f32, 77825).endswith("true, false>")            # unaligned stride
+    assert row_kernel_name(f32, 77823).startswith("dppo::rows_stream<float")
+    assert row_kernel_name(f32, 151936, with_dlogits=False).startswith("dppo::rows_stream<float")
     # two row buffers for the bf16 backward shapes 512 x 4 .. 1024 x 8 only
     assert row_kernel_name(bf, 32000) == "dppo::rows_bf16_resident_db<512, 8>"
     assert row_kernel_name(bf, 65536) == "dppo::rows_bf16_resident_db<1024, 8>"

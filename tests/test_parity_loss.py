@@ -189,6 +189,8 @@ RESIDENT_CASES = [
     (torch.float32, 16000, 1400, "rows_f32_resident<512, 8, true>"),
     (torch.float32, 24000, 700, "rows_f32_resident<1024, 6, true>"),
     (torch.float32, 76000, 700, "rows_f32_resident<1024, 19, true>"),
+    # longer fp32 rows: resident prefix, streamed tail
+    (torch.float32, 155656, 600, "rows_f32_prefix<1024, 19>"),
 ]
 
 
@@ -218,6 +220,48 @@ def test_every_resident_shape_several_rows_per_workgroup(dtype, V, T, kernel):
     diff = np.abs(st.astype(np.int64) - np.asarray(ref["stats"], np.int64))
     assert diff[0] == 0 and diff[4] == 0 and np.all(diff <= n_ties), (st, ref["stats"], n_ties)
     assert st[4] == int(((ids.cpu().numpy() > V) & (mask.cpu().numpy() != 0)).sum()) > 0
+
+
+@pytest.mark.parametrize("V,ld,T", [(77825, 77828, 500), (151937, 151940, 500),
+                                    (151936, 151936, 7)])
+def test_fp32_prefix_kernel_ragged_ends_and_strides(V, ld, T):
+    """fp32 rows past the resident kernels with 16-byte-aligned strides: the resident-prefix
+    kernel, with a ragged last chunk (V % 4 != 0) that one thread reads and writes element
+    by element, a prefix that is the whole row but that end (V = 77825), in place and into a
+    separate buffer, several rows per workgroup with masked rows and bad ids in between."""
+    _say("fp32 prefix", V, ld, T)
+    assert P.row_kernel_name(torch.float32, V, ld) == "dppo::rows_f32_prefix<1024, 19>"
+    g = torch.Generator(device=DEV).manual_seed(V + T)
+    zbuf = torch.full((T, ld), float("nan"), device=DEV)
+    z = zbuf[:, :V]
+    z.copy_(torch.randn(T, V, generator=g, device=DEV) * 3)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[0] = V - 1                                      # in the ragged end
+    ids[min(2, T - 1)] = 5
+    if T > 40:
+        ids[7::97] = V + 1                              # bad ids on valid rows
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    mask[3::11] = 0
+    anchor = oracle_anchor(z, ids.clamp(0, V - 1)).to(DEV)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.3 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    dbuf = torch.full((T, ld), 7.0, device=DEV)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, scale_mode="const",
+                                       dlogits=dbuf[:, :V])
+    torch.cuda.synchronize()
+    compare_loss(res, ref, params, torch.float32)
+    assert torch.all(dbuf[:, V:] == 7.0), "stores past the row"
+    fl = res.flags.cpu().numpy()
+    np.testing.assert_array_equal(res.stats.cpu().numpy(), oracle.stats_of(fl, params))
+    inpl = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, scale_mode="const",
+                                        dlogits=z)
+    torch.cuda.synchronize()
+    assert torch.equal(z.view(torch.int32), res.dlogits.view(torch.int32)), "in place"
+    assert torch.equal(inpl.logp.view(torch.int32), res.logp.view(torch.int32))
+    assert torch.isnan(zbuf[:, V:]).all()
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
