@@ -366,9 +366,10 @@ def cpu_model() -> str:
 def timed_steps(step, steps, dev, flush_bytes):
     """Time `steps` steps. Without a flush: back to back between two events, mean per step,
     and the library's events around the per-row kernel (mean per launch). With a flush: a
-    flush_bytes buffer is written before every step (outside its events), which evicts the
-    previous step's data from the 256 MB Infinity Cache, and the medians of the per-step and
-    per-launch times are returned."""
+    flush_bytes buffer is read before every step (outside its events), which evicts the
+    previous step's data from the 256 MB Infinity Cache without leaving dirty lines to write
+    back during the step, and the medians of the per-step and per-launch times are
+    returned."""
     stream = torch.cuda.current_stream(dev)
     if flush_bytes <= 0:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -381,10 +382,10 @@ def timed_steps(step, steps, dev, flush_bytes):
             torch.cuda.synchronize()
             k_ms_total, k_launches = kt.read()
         return e0.elapsed_time(e1) / steps, k_ms_total / max(1, k_launches), "mean"
-    buf = torch.empty(flush_bytes // 4, dtype=torch.float32, device=dev)
+    buf = torch.ones(flush_bytes // 4, dtype=torch.float32, device=dev)
     per_step, per_kernel = [], []
-    for i in range(steps):
-        buf.fill_(float(i))
+    for _ in range(steps):
+        buf.sum()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         with P.KernelTimer() as kt:
