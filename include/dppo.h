@@ -221,7 +221,11 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
  *  workspace    device buffer of at least fused_lm_head_workspace_bytes(T, d, V, vocab_chunk)
  *               bytes, 256-byte aligned, owned by the caller; its contents are scratch.
  * Masked rows and bad ids behave as in the row entry point (their G rows are zero). The
- * computation of rows with loss mask 0 is not skipped. The call allocates nothing.
+ * computation of rows with loss mask 0 is not skipped: a caller whose batch has many of them
+ * passes only the rows it trains on (hidden, ids and the per-token inputs gathered), which
+ * gives the same loss, counters and token-mean scale, and dweight up to the order of its
+ * sum over tokens; the dhidden rows of the dropped tokens are zero. The call allocates
+ * nothing.
  */
 dppo_status fused_lm_head_loss_fwd_bwd(
     const void* hidden, const void* weight, int32_t dtype, int64_t T, int64_t d, int64_t V,
