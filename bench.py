@@ -257,16 +257,16 @@ def vocab_shard_measure(dev, wl, lp_mu, lp_ref, n_shards=8, reps=20):
             "tokens_per_s": round(T / ((c_stats + c_loss) * 1e-3), 1)}
 
 
-def fp32_rows_measure(dev, T=8192, V=151936, reps=10):
-    """fp32 logits with rows longer than the register-resident kernels hold: T = 8192,
-    V = 151936 (N(0, 3^2), uniform token ids, every token valid), the fused forward and
-    backward. Timed by the library's events around the per-row kernel (the resident-prefix
-    kernel); algorithmic bytes as for the bf16 rows (logits read once, dlogits written
-    once, 29 B of per-token vectors)."""
+def long_rows_measure(dev, dtype=torch.float32, T=8192, V=151936, reps=10, key="fp32_rows"):
+    """Rows longer than the register-resident kernels hold (fp32 past 77824 entries, bf16 past
+    155648): N(0, 3^2) logits of `dtype`, uniform token ids, every token valid, the fused
+    forward and backward. Timed by the library's events around the per-row kernel (the
+    resident-prefix kernel); algorithmic bytes as for the flagship rows (logits read once,
+    dlogits written once, 29 B of per-token vectors)."""
     g = torch.Generator(device=dev).manual_seed(7)
-    z = torch.empty(T, V, dtype=torch.float32, device=dev)
+    z = torch.empty(T, V, dtype=dtype, device=dev)
     for a in range(0, T, 1024):
-        z[a:a + 1024] = 3.0 * torch.randn(min(1024, T - a), V, generator=g, device=dev)
+        z[a:a + 1024] = (3.0 * torch.randn(min(1024, T - a), V, generator=g, device=dev)).to(dtype)
     ids = torch.randint(0, V, (T,), generator=g, device=dev)
     anchor = anchor_logprob(z, ids)
     lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=dev, dtype=torch.float64)).float()
@@ -289,15 +289,17 @@ def fp32_rows_measure(dev, T=8192, V=151936, reps=10):
         k_ms, k_n = kt.read()
     call_ms = e0.elapsed_time(e1) / reps
     ms = k_ms / max(1, k_n)
-    b_alg = algorithmic_bytes(T, V, T, 4, 29)
+    esize = torch.finfo(dtype).bits // 8
+    b_alg = algorithmic_bytes(T, V, T, esize, 29)
     gbps = b_alg / (ms * 1e-3) / 1e9
     del z, dl, out
+    name = "fp32" if dtype == torch.float32 else "bf16"
     return {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(gbps / HBM_PEAK_GBPS, 4),
-            "kernel": P.row_kernel_name(torch.float32, V), "kernel_ms": round(ms, 4),
-            "alg_bytes_per_launch": b_alg, "workload": f"fp32 rows T={T} V={V}",
+            "kernel": P.row_kernel_name(dtype, V), "kernel_ms": round(ms, 4),
+            "alg_bytes_per_launch": b_alg, "workload": f"{name} rows T={T} V={V}",
             "call_ms": round(call_ms, 4), "tokens_per_s": round(T / (call_ms * 1e-3), 1),
-            "traffic": recorded_traffic("fp32_rows")}
+            "traffic": recorded_traffic(key)}
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak, AMD specification
@@ -420,8 +422,10 @@ def main():
                     help="skip the versioned log-prob measurement")
     ap.add_argument("--no-fp32", action="store_true",
                     help="skip the fp32 long-row measurement")
+    ap.add_argument("--no-bf16-long", action="store_true",
+                    help="skip the bf16 long-row measurement (V = 262144)")
     ap.add_argument("--flush-mb", type=int, default=-1,
-                    help="write this many MB before every timed step and report medians "
+                    help="read this many MB before every timed step and report medians "
                          "(default: 512 for tiny and small_vocab, whose working set fits the "
                          "256 MB Infinity Cache; 0 otherwise)")
     args = ap.parse_args()
@@ -511,7 +515,11 @@ def main():
         result["versioned_logprob_roofline"] = vr
     if not args.no_fp32 and args.workload == "large_vocab":
         log("fp32 long rows")
-        result["fp32_rows_roofline"] = fp32_rows_measure(dev)
+        result["fp32_rows_roofline"] = long_rows_measure(dev)
+    if not args.no_bf16_long and args.workload == "large_vocab":
+        log("bf16 long rows")
+        result["bf16_long_rows_roofline"] = long_rows_measure(
+            dev, torch.bfloat16, T=8192, V=262144, key="bf16_long_rows")
     if args.ewma_elems > 0:
         result["ewma_roofline"] = ewma_bandwidth(dev, args.ewma_elems)
     if not args.no_lm_head:

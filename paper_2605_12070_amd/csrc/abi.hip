@@ -265,7 +265,7 @@ const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t w
   const char* ty = dtype == DPPO_BF16 ? "bf16" : "f32";
   const char* bw = with_dlogits ? "true" : "false";
   if (L.prefix)
-    snprintf(buf, sizeof(buf), "dppo::rows_f32_prefix<%d, %d>", L.threads, L.chunks);
+    snprintf(buf, sizeof(buf), "dppo::rows_%s_prefix<%d, %d>", ty, L.threads, L.chunks);
   else if (L.resident && dtype == DPPO_BF16 && !with_dlogits)
     snprintf(buf, sizeof(buf), "dppo::rows_bf16_fwd<%d, %d>", L.threads, L.chunks);
   else if (L.two_buffers)

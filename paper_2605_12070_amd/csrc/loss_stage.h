@@ -65,10 +65,10 @@ struct RowLaunch {
   bool resident = false;
   bool persistent = false;  // grid = resident workgroups on the device, rows looped over
   bool two_buffers = false; // resident backward kernel with two row buffers
-  bool prefix = false;       // fp32 backward kernel with a resident prefix and a streamed tail
+  bool prefix = false;       // backward kernel with a resident prefix and a streamed tail
 };
 
-constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the fp32 prefix kernel
+constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the prefix kernels
 
 RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force);
 void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream_t st);

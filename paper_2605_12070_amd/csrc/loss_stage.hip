@@ -735,16 +735,18 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgsOf<BWD> a) {
 // Pass A streams the tail four chunks per thread at a time (chunks NT NC + tid, + NT, ...;
 // the last may be partial) and merges each as a general (max, sum) partial, then loads the
 // resident chunks and gives them one shift per thread, as the resident kernel does. Pass B
-// scales the resident exponentials into dlogits, then re-reads the tail. Element e of the row is read and written by the same thread, so dlogits may alias
-// the logits.
+// scales the resident exponentials into dlogits, then re-reads the tail. Element e of the
+// row is read and written by the same thread, so dlogits may alias the logits.
 // ---------------------------------------------------------------------------------------
-template <int NT>
+template <typename Tin, int NT>
 __device__ void skip_row_long(const RowArgs& a, int64_t row, bool valid, StatCount& sc) {
-  using C = Chunk<float, true>;
+  using C = Chunk<Tin, true>;
   if (a.dlogits) {
-    float* d = (float*)a.dlogits + row * a.ldd;
-    const int nchunk = (a.V + 3) >> 2;
-    const float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    Tin* d = (Tin*)a.dlogits + row * a.ldd;
+    const int nchunk = (a.V + C::E - 1) / C::E;
+    float z[C::E];
+#pragma unroll
+    for (int j = 0; j < C::E; ++j) z[j] = 0.0f;
     for (int idx = threadIdx.x; idx < nchunk; idx += NT) C::store(d, idx, a.V, z);
   }
   if (threadIdx.x == 0) {
@@ -770,7 +772,7 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
     const int64_t y = uload(a.ids + row);
     const bool good = (y >= 0) && (y < V);
     if (!(valid && good)) {               // uniform
-      skip_row_long<NT>(a, row, valid, sc);
+      skip_row_long<float, NT>(a, row, valid, sc);
       continue;
     }
     const float* zrow = (const float*)a.logits + row * a.ld;
@@ -887,6 +889,176 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
     if (rag_owner) {
       for (int e = nfull * 4; e < V; ++e)
         drow[e] = (e == y) ? dy : w * exp2_hw(__builtin_fmaf(zrow[e], kLog2e, -l2));
+    }
+  }
+  if (threadIdx.x == 0) flush_stats(a, sc);
+}
+
+// ---------------------------------------------------------------------------------------
+// bf16 rows with dlogits that are longer than the register-resident kernels hold
+// (V > 8 NT NC): the first NT x NC 16-byte chunks of a row stay in registers between the two
+// passes with the numerics of rows_bf16_resident (an integer log2 shift per chunk, kept in
+// LDS, and the exponentials stored in place as fp16 pairs); the rest of the row (the tail)
+// is read a second time and its gradient formed in fp32 from the logits. Per row: V elements
+// read, V - 8 NT NC read again, V written, against 2 V read and V written by the streaming
+// kernel. Persistent, one workgroup per row at a time; pass A streams the tail first, so
+// that its registers and the resident chunks are never live together. Element e of the row
+// is read and written by the same thread, so dlogits may alias the logits.
+// ---------------------------------------------------------------------------------------
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
+  constexpr int P = NT * NC;              // resident chunks of a row
+  constexpr int U = 4;                    // tail chunks per thread in flight
+  __shared__ float red[2 * (NT / 64) + 2];
+  __shared__ Bcast bc;
+  __shared__ float nch[NC][NT];           // per-chunk shifts, [c][tid]: conflict-free
+  StatCount sc;
+  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
+    const int tid = threadIdx.x;
+    const int V = a.V;
+    const int nfull = V >> 3;             // whole 16-byte chunks, >= P by the selection
+    const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
+    const int64_t y = uload(a.ids + row);
+    const bool good = (y >= 0) && (y < V);
+    if (!(valid && good)) {               // uniform
+      skip_row_long<uint16_t, NT>(a, row, valid, sc);
+      continue;
+    }
+    const uint16_t* zrow = (const uint16_t*)a.logits + row * a.ld;
+    float zy = 0.0f;
+    if (tid == 0) zy = bf16_to_f32(zrow[y]);
+    // Whole chunks through a resource over the row: a chunk past the end (offset kOff)
+    // loads zeros, replaced by -inf below. The V % 8 last elements belong to one thread.
+    const __amdgpu_buffer_rsrc_t rz = row_rsrc(zrow, nfull * 16);
+    constexpr int kOff = 0x7fffff00;
+    const bool rag_owner = (V & 7) != 0 && tid == nfull % NT;
+    // pass A, tail: general (max, sum) partials per chunk
+    float nt = -INFINITY, st = 0.0f;
+    for (int i0 = P + tid; i0 < nfull; i0 += U * NT) {
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = i0 + u * NT;
+        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bool in = i0 + u * NT < nfull;
+        float x[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          x[2 * k] = in ? bf16_lo(v[u][k]) : -INFINITY;
+          x[2 * k + 1] = in ? bf16_hi(v[u][k]) : -INFINITY;
+        }
+        const float m = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
+        const float ns = (m == -INFINITY) ? 0.0f : m * kLog2e;
+        float cs = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cs += exp2_hw(__builtin_fmaf(x[j], kLog2e, -ns));
+        merge_ns(nt, st, (m == -INFINITY) ? -INFINITY : ns, cs);
+      }
+    }
+    if (rag_owner) {
+      for (int e = nfull * 8; e < V; ++e) {
+        const float x = bf16_to_f32(zrow[e]);
+        const float ns = (x == -INFINITY) ? 0.0f : x * kLog2e;
+        merge_ns(nt, st, (x == -INFINITY) ? -INFINITY : ns, exp2_hw(__builtin_fmaf(x, kLog2e, -ns)));
+      }
+    }
+    // pass A, resident chunks: shift n_c = ceil(L max(chunk)), fp16 exponentials in place
+    uint32_t r[NC][4];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) load16(r[c], rz, tid * 16, c * NT * 16);
+    float N = -INFINITY, S = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      float x[8];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x[2 * k] = bf16_lo(r[c][k]);
+        x[2 * k + 1] = bf16_hi(r[c][k]);
+      }
+      const float cm = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
+      const float nc = __builtin_ceilf(cm * kLog2e);
+      const float sh = (nc == -INFINITY) ? 0.0f : nc;
+      float e[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) e[j] = exp2_hw(__builtin_fmaf(x[j], kLog2e, -sh));
+      const float cs = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        r[c][k] = pack_f16(e[2 * k], e[2 * k + 1]);
+        asm volatile("" : "+v"(r[c][k]));
+      }
+      nch[c][tid] = nc;
+      merge_ns_int(N, S, nc, cs);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    merge_ns(N, S, nt, st);
+    block_merge_ns<NT>(N, S, red);
+    const float lse2 = (N == -INFINITY) ? __builtin_nanf("") : N + log2f(S);
+    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    if (!a.dlogits) continue;             // uniform
+    __syncthreads();
+    const float w = bc.w;
+    const float dy = bc.dy;
+    const float l2 = bc.lse2;
+    uint16_t* drow = (uint16_t*)a.dlogits + row * a.ldd;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
+    // pass B, resident chunks: w 2^(n_c - lse2) e (the sampled entry: the thread that holds
+    // it); a NaN lse (non-finite row) makes every element NaN
+    const int cy = (int)(y >> 3);
+    const int jy = (int)(y & 7);
+    const int my_slot = (cy < P && cy % NT == tid) ? cy / NT : -1;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float ncv = nch[c][tid];
+      const float f = (l2 != l2) ? l2 : ((ncv == -INFINITY) ? 0.0f : w * exp2_hw(ncv - l2));
+      float o[8];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        o[2 * k] = f16_lo_mul(r[c][k], f);
+        o[2 * k + 1] = f16_hi_mul(r[c][k], f);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = (c == my_slot && j == jy) ? dy : o[j];
+      u32x4 v;
+      v.x = pack_bf16(o[0], o[1]);
+      v.y = pack_bf16(o[2], o[3]);
+      v.z = pack_bf16(o[4], o[5]);
+      v.w = pack_bf16(o[6], o[7]);
+      buf_store16_nt(v, rd, tid * 16, c * NT * 16);
+    }
+    // pass B, tail: re-read, w 2^(z L - lse2), store (stores past the row are dropped)
+    for (int i0 = P + tid; i0 < nfull; i0 += U * NT) {
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = i0 + u * NT;
+        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int idx = i0 + u * NT;
+        float o[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          o[2 * k] = w * exp2_hw(__builtin_fmaf(bf16_lo(v[u][k]), kLog2e, -l2));
+          o[2 * k + 1] = w * exp2_hw(__builtin_fmaf(bf16_hi(v[u][k]), kLog2e, -l2));
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = (idx == cy && j == jy) ? dy : o[j];
+        u32x4 ov;
+        ov.x = pack_bf16(o[0], o[1]);
+        ov.y = pack_bf16(o[2], o[3]);
+        ov.z = pack_bf16(o[4], o[5]);
+        ov.w = pack_bf16(o[6], o[7]);
+        buf_store16_nt(ov, rd, idx < nfull ? idx * 16 : kOff, 0);
+      }
+    }
+    if (rag_owner) {
+      for (int e = nfull * 8; e < V; ++e)
+        drow[e] = to_bf16((e == y) ? dy : w * exp2_hw(__builtin_fmaf(bf16_to_f32(zrow[e]), kLog2e, -l2)));
     }
   }
   if (threadIdx.x == 0) flush_stats(a, sc);
@@ -1070,11 +1242,11 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   }
   L.threads = 1024;
   L.resident = false;
-  if (dtype == DPPO_F32 && bwd && aligned && force != kForceStream &&
-      V / 4 >= (int64_t)1024 * kPrefixNC) {
-    // longer fp32 rows: a resident prefix of 1024 x kPrefixNC whole chunks, the rest (and a
+  if (bwd && aligned && force != kForceStream && (V * esize) / 16 >= (int64_t)1024 * kPrefixNC) {
+    // longer rows: a resident prefix of 1024 x kPrefixNC whole chunks, the rest (and a
     // ragged end) streamed twice
-    L.fn = (const void*)rows_f32_prefix<1024, kPrefixNC>;
+    L.fn = dtype == DPPO_F32 ? (const void*)rows_f32_prefix<1024, kPrefixNC>
+                             : (const void*)rows_bf16_prefix<1024, kPrefixNC>;
     L.chunks = kPrefixNC;
     L.prefix = true;
     L.persistent = true;

@@ -304,13 +304,19 @@ def test_host_ewma_proxy_decisions_follow_the_library(monkeypatch):
 
 def test_row_kernel_name_follows_the_selection_rule():
     """Host-only query: the resident kernel while a row fits NT x NC 16-byte chunks (at most
-    1024 x 19 x 8 = 155648 bf16 elements) with whole chunks, the streaming kernel beyond."""
+    1024 x 19 x 8 = 155648 bf16 elements) with whole chunks; beyond, the resident-prefix
+    kernel for aligned rows with dlogits, the streaming kernel otherwise."""
     import torch
     from paper_2605_12070_amd import row_kernel_name
     bf, f32 = torch.bfloat16, torch.float32
     assert row_kernel_name(bf, 151936) == "dppo::rows_bf16_resident<1024, 19, true>"
     assert row_kernel_name(bf, 155648) == "dppo::rows_bf16_resident<1024, 19, true>"
-    assert row_kernel_name(bf, 155656).startswith("dppo::rows_stream<unsigned short, 1024, true")
+    # longer bf16 rows with dlogits: a resident prefix and a streamed tail
+    assert row_kernel_name(bf, 155656) == "dppo::rows_bf16_prefix<1024, 19>"
+    assert row_kernel_name(bf, 155649, ld=155656) == "dppo::rows_bf16_prefix<1024, 19>"
+    assert row_kernel_name(bf, 262144) == "dppo::rows_bf16_prefix<1024, 19>"
+    assert row_kernel_name(bf, 155649).endswith("true, false>")             # unaligned stride
+    assert row_kernel_name(bf, 262144, with_dlogits=False).startswith("dppo::rows_stream<unsigned short, 1024, false")
     assert row_kernel_name(bf, 151936, with_dlogits=False) == "dppo::rows_bf16_fwd<1024, 19>"
     assert row_kernel_name(f32, 32000, with_dlogits=False) == "dppo::rows_f32_resident<1024, 8, false>"
     assert row_kernel_name(bf, 2048) == "dppo::rows_bf16_resident<256, 1, true>"

@@ -189,8 +189,9 @@ RESIDENT_CASES = [
     (torch.float32, 16000, 1400, "rows_f32_resident<512, 8, true>"),
     (torch.float32, 24000, 700, "rows_f32_resident<1024, 6, true>"),
     (torch.float32, 76000, 700, "rows_f32_resident<1024, 19, true>"),
-    # longer fp32 rows: resident prefix, streamed tail
+    # longer rows: resident prefix, streamed tail
     (torch.float32, 155656, 600, "rows_f32_prefix<1024, 19>"),
+    (torch.bfloat16, 180000, 600, "rows_bf16_prefix<1024, 19>"),
 ]
 
 
@@ -260,6 +261,51 @@ def test_fp32_prefix_kernel_ragged_ends_and_strides(V, ld, T):
                                         dlogits=z)
     torch.cuda.synchronize()
     assert torch.equal(z.view(torch.int32), res.dlogits.view(torch.int32)), "in place"
+    assert torch.equal(inpl.logp.view(torch.int32), res.logp.view(torch.int32))
+    assert torch.isnan(zbuf[:, V:]).all()
+
+
+@pytest.mark.parametrize("V,ld,T", [(155649, 155656, 300), (262147, 262152, 300),
+                                    (262144, 262144, 7)])
+def test_bf16_prefix_kernel_ragged_ends_and_strides(V, ld, T):
+    """bf16 rows past the resident kernels (more than 1024 x 19 x 8 = 155648 entries) with
+    16-byte-aligned strides: the resident-prefix kernel, with a ragged last chunk (V % 8 != 0)
+    that one thread reads and writes element by element, a prefix that is the whole row but
+    one entry (V = 155649), the sampled id in the resident part, in the streamed tail and in
+    the ragged end, in place and into a separate buffer, several rows per workgroup with
+    masked rows and bad ids in between."""
+    _say("bf16 prefix", V, ld, T)
+    assert P.row_kernel_name(torch.bfloat16, V, ld) == "dppo::rows_bf16_prefix<1024, 19>"
+    g = torch.Generator(device=DEV).manual_seed(V + T)
+    zbuf = torch.full((T, ld), float("nan"), device=DEV, dtype=torch.bfloat16)
+    z = zbuf[:, :V]
+    z.copy_((torch.randn(T, V, generator=g, device=DEV) * 3).to(torch.bfloat16))
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[0] = V - 1                                      # in the ragged end (or the tail)
+    ids[min(2, T - 1)] = 5                              # in the resident part
+    ids[min(4, T - 1)] = 160000 if V > 160000 else V - 2   # in the streamed tail
+    if T > 40:
+        ids[7::97] = V + 1                              # bad ids on valid rows
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    mask[3::11] = 0
+    anchor = oracle_anchor(z, ids.clamp(0, V - 1)).to(DEV)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.3 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    dbuf = torch.full((T, ld), 7.0, device=DEV, dtype=torch.bfloat16)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, scale_mode="const",
+                                       dlogits=dbuf[:, :V])
+    torch.cuda.synchronize()
+    compare_loss(res, ref, params, torch.bfloat16)
+    assert torch.all(dbuf[:, V:] == 7.0), "stores past the row"
+    fl = res.flags.cpu().numpy()
+    np.testing.assert_array_equal(res.stats.cpu().numpy(), oracle.stats_of(fl, params))
+    inpl = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, scale_mode="const",
+                                        dlogits=z)
+    torch.cuda.synchronize()
+    assert torch.equal(z.view(torch.int16), res.dlogits.view(torch.int16)), "in place"
     assert torch.equal(inpl.logp.view(torch.int32), res.logp.view(torch.int32))
     assert torch.isnan(zbuf[:, V:]).all()
 
