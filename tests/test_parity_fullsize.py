@@ -116,6 +116,17 @@ def test_large_vocab_fullsize():
     _check_workload(wl, lp_ref, lp_mu, lp_ref.cpu().double().numpy())
 
 
+def test_bf16_long_rows_fullsize():
+    """bf16 rows past the resident kernels at the benchmark's long-row size (T = 8192,
+    V = 262144): the resident-prefix kernel with the large-vocabulary recipe, sampled rows
+    against the oracle and the row properties on every row."""
+    wl = W.make_workload("large_vocab", device=DEV, T=8192, V=262144, seed=12)
+    assert P.row_kernel_name(torch.bfloat16, wl.V) == "dppo::rows_bf16_prefix<1024, 19>"
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    _check_workload(wl, lp_ref, lp_mu, lp_ref.cpu().double().numpy())
+
+
 def test_long_agentic_fullsize():
     wl = W.make_workload("long_agentic", device=DEV)
     anchor = torch_anchor(wl.logits, wl.ids)
