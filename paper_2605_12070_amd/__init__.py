@@ -597,3 +597,30 @@ class DecoupledPPOLoss(torch.autograd.Function):
     def backward(ctx, g_loss, g_lp, g_stats):
         (d,) = ctx.saved_tensors
         return (d * g_loss.to(d.dtype), None, None, None, None, None, None, None)
+
+
+class FusedLMHeadLoss(torch.autograd.Function):
+    """Autograd wrapper of the fused LM head: forward runs fused_lm_head_loss_fwd_bwd (the
+    loss and both gradients at once, logits never materialised); backward returns
+    grad_output * dL/dhidden and grad_output * dL/dweight in the dtypes of hidden and weight
+    (one extra elementwise pass each)."""
+
+    @staticmethod
+    def forward(ctx, hidden, weight, token_ids, logp_mu_old, logp_ref, advantages, loss_mask,
+                token_scale, kwargs):
+        res = fused_lm_head_loss_fwd_bwd(hidden.detach(), weight.detach(), token_ids,
+                                         logp_mu_old, logp_ref, advantages, loss_mask,
+                                         token_scale, want_grads=True, **(kwargs or {}))
+        ctx.save_for_backward(res.dhidden, res.dweight)
+        ctx.dtypes = (hidden.dtype, weight.dtype)
+        ctx.mark_non_differentiable(res.logp, res.stats)
+        return res.loss[0], res.logp, res.stats
+
+    @staticmethod
+    def backward(ctx, g_loss, g_lp, g_stats):
+        dh, dw = ctx.saved_tensors
+        th, tw = ctx.dtypes
+        gh = (dh * g_loss).to(th) if ctx.needs_input_grad[0] else None
+        gw = (dw * g_loss).to(tw) if ctx.needs_input_grad[1] else None
+        return (gh, gw, None, None, None, None, None, None, None)
+

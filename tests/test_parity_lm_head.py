@@ -279,3 +279,28 @@ def test_lm_head_fullsize_few_valid_tokens_every_gradient_entry(vocab_chunk):
     err = np.abs(dh[rows] - dh_ref)
     assert np.all(err <= dh_bound + 1e-7), f"dhidden: worst excess {np.max(err - dh_bound - 1e-7):.3e}"
     _say("lm_head 64 valid ok", vocab_chunk, "worst dW err / bound", round(worst, 4))
+
+
+def test_lm_head_autograd_wrapper_returns_the_call_gradients():
+    """FusedLMHeadLoss: loss.backward() gives hidden.grad and weight.grad equal to the direct
+    call's dhidden and dweight times the upstream gradient, in the parameters' dtype."""
+    T, d, V = 300, 64, 1000
+    print(f"[case] lm head autograd T={T} d={d} V={V}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(31)
+    hidden = torch.randn(T, d, generator=g, device=DEV).to(torch.bfloat16)
+    weight = (0.1 * torch.randn(V, d, generator=g, device=DEV)).to(torch.bfloat16)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    lp_ref = torch.full((T,), -7.0, device=DEV)
+    lp_mu = lp_ref + 0.05 * torch.randn(T, generator=g, device=DEV)
+    adv = torch.randn(T, generator=g, device=DEV)
+    direct = P.fused_lm_head_loss_fwd_bwd(hidden, weight, ids, lp_mu, lp_ref, adv)
+    h = hidden.clone().requires_grad_(True)
+    w = weight.clone().requires_grad_(True)
+    loss, lp, st = P.FusedLMHeadLoss.apply(h, w, ids, lp_mu, lp_ref, adv, None, None, None)
+    (3.0 * loss).backward()
+    torch.cuda.synchronize()
+    assert torch.equal(loss.detach(), direct.loss[0]) and torch.equal(lp, direct.logp)
+    assert h.grad.dtype == torch.bfloat16 and w.grad.dtype == torch.bfloat16
+    assert torch.equal(h.grad, (3.0 * direct.dhidden).to(torch.bfloat16))
+    assert torch.equal(w.grad, (3.0 * direct.dweight).to(torch.bfloat16))
+
