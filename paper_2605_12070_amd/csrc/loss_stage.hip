@@ -183,7 +183,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     const __amdgpu_buffer_rsrc_t rz =
         row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
 #pragma unroll
-    for (int c = 0; c < NC; ++c) load16(r1[c], rz, threadIdx.x * 16, c * NT * 16);
+    for (int c = 0; c < NC; ++c) load16<kAuxLast>(r1[c], rz, threadIdx.x * 16, c * NT * 16);
   }
   int parity = 0;
   // One row: its chunks are in r (cur); nx receives the next row's chunks (nx is r itself
@@ -214,7 +214,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
         row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
     if constexpr (DB) {
 #pragma unroll
-      for (int c = 0; c < NC; ++c) load16(nx[c], rn, voff, c * NT * 16);
+      for (int c = 0; c < NC; ++c) load16<kAuxLast>(nx[c], rn, voff, c * NT * 16);
     }
     const int64_t y = uload(a.ids + row);
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
@@ -329,7 +329,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     // make every wait in the next row's pass A also wait for store acknowledgements.
     if constexpr (!DB) {
 #pragma unroll
-      for (int c = 0; c < NC; ++c) load16(nx[c], rn, voff, c * NT * 16);
+      for (int c = 0; c < NC; ++c) load16<kAuxLast>(nx[c], rn, voff, c * NT * 16);
     }
     if (want_d && !rd_cur) {                // zeros for a row that was not read
       const __amdgpu_buffer_rsrc_t rz = row_rsrc(drow, V * 2);
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
     const __amdgpu_buffer_rsrc_t rz =
         row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
 #pragma unroll
-    for (int c = 0; c < NC; ++c) load16(r[c], rz, threadIdx.x * 16, c * NT * 16);
+    for (int c = 0; c < NC; ++c) load16<kAuxLast>(r[c], rz, threadIdx.x * 16, c * NT * 16);
   }
   int parity = 0;                          // flips after each merge that ran
   for (; row < a.T; row += gridDim.x) {
@@ -437,7 +437,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
         x[2 * k] = bf16_lo(r[c][k]);
         x[2 * k + 1] = bf16_hi(r[c][k]);
       }
-      load16(r[c], rn, voff, c * NT * 16);
+      load16<kAuxLast>(r[c], rn, voff, c * NT * 16);
       const float cm = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
       float nc = __builtin_ceilf(cm * kLog2e);
       const float sh = (nc == -INFINITY) ? 0.0f : nc;
@@ -501,7 +501,7 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
     float r[NC][4];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      const u32x4 v = buf_load16(rz, voff, c * NT * 16);
+      const u32x4 v = buf_load16<kAuxLast>(rz, voff, c * NT * 16);
 #pragma unroll
       for (int j = 0; j < 4; ++j) r[c][j] = __uint_as_float(v[j]);
     }
@@ -818,7 +818,7 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
     float r[NC][4];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      const u32x4 v = buf_load16(rz, tid * 16, c * NT * 16);
+      const u32x4 v = buf_load16<kAuxLast>(rz, tid * 16, c * NT * 16);
 #pragma unroll
       for (int j = 0; j < 4; ++j) r[c][j] = __uint_as_float(v[j]);
     }
@@ -870,7 +870,7 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int idx = i0 + u * NT;
-        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+        v[u] = buf_load16<kAuxLast>(rz, idx < nfull ? idx * 16 : kOff, 0);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -968,7 +968,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
     // pass A, resident chunks: shift n_c = ceil(L max(chunk)), fp16 exponentials in place
     uint32_t r[NC][4];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) load16(r[c], rz, tid * 16, c * NT * 16);
+    for (int c = 0; c < NC; ++c) load16<kAuxLast>(r[c], rz, tid * 16, c * NT * 16);
     float N = -INFINITY, S = 0.0f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -1035,7 +1035,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int idx = i0 + u * NT;
-        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+        v[u] = buf_load16<kAuxLast>(rz, idx < nfull ? idx * 16 : kOff, 0);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {

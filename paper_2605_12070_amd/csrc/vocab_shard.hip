@@ -56,7 +56,7 @@ __device__ __forceinline__ void row_partial(const char* row, int Vs, float& N, f
     for (int c0 = 0; c0 < nfull; c0 += kNT * kGroup) {
       u32x4 v[kGroup];
 #pragma unroll
-      for (int g = 0; g < kGroup; ++g) v[g] = buf_load16(rz, (c0 + g * kNT + tid) * 16, 0);
+      for (int g = 0; g < kGroup; ++g) v[g] = buf_load16<kAuxLast>(rz, (c0 + g * kNT + tid) * 16, 0);
 #pragma unroll
       for (int g = 0; g < kGroup; ++g) {
         if (c0 + g * kNT + tid >= nfull) continue;
