@@ -78,7 +78,6 @@ std::pair<hipEvent_t, hipEvent_t>* timer_slot() {
 
 // Workgroups of `fn` that fit on the current device at once (CUs x per-CU occupancy),
 // cached per (device, kernel).
-constexpr int64_t kPersistentFill = 27;  // out of 32 resident slots
 
 hipError_t resident_slots(const dppo::RowLaunch& L, int64_t* slots) {
   static std::mutex mu;
@@ -110,9 +109,9 @@ dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgsV& args, in
     int64_t slots = 0;
     const hipError_t oe = resident_slots(L, &slots);
     if (oe != hipSuccess) return hip_fail(oe, "occupancy query");
-    // 27 of every 32 slots: with every CU streaming, the row kernel moves fewer bytes per
-    // second than with about 27 per 32-CU XCD (measured on MI355X at V = 151936).
-    slots = slots * kPersistentFill / 32;
+    // L.fill of every 32 slots: with every CU streaming, a row kernel moves fewer bytes per
+    // second than with a few CUs of each 32-CU XCD idle (the fill is chosen per kernel).
+    slots = slots * L.fill / 32;
     if (slots < 1) slots = 1;
     if (slots < grid) grid = slots;
   }

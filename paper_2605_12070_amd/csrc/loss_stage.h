@@ -66,6 +66,7 @@ struct RowLaunch {
   bool persistent = false;  // grid = resident workgroups on the device, rows looped over
   bool two_buffers = false; // resident backward kernel with two row buffers
   bool prefix = false;       // backward kernel with a resident prefix and a streamed tail
+  int fill = 27;             // persistent grids: workgroups launched per 32 resident slots
 };
 
 constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the prefix kernels

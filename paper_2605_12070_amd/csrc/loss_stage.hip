@@ -1155,6 +1155,24 @@ constexpr bool kResidentDB[kNumResident] = {false, false, false, true, true,
                                             true,  true,  true,  false, false};
 constexpr bool kF32Persistent[kNumResident] = {true,  true,  true,  true,  true,
                                                true,  false, false, false, true};
+// Persistent grids launch kFill* of every 32 resident workgroup slots. A gradient kernel
+// moves fewer bytes per second with every CU streaming than with a few CUs of each XCD
+// idle; the read-only forward kernels mostly want every slot. Same-box A/B at T = 16384 over
+// fills of 24 to 32, per kernel and shape (the shapes not listed as measured take a measured
+// neighbour's value): the flagship (bf16 backward 1024 x 19) is fastest at 27 (29-32: 2-3 %
+// slower, 25: 3 %); the forward kernel at 32 for 512 x 4 .. 1024 x 8 (7-13 % faster than
+// 27) and 30 for 1024 x 12 and 19 (6 %, 3 %); the long-row prefix kernels at 31 (bf16, 6 %)
+// and 32 (fp32, 2 %).
+// Shapes:                                   256x1 256x2 256x4 512x4 512x6 512x8 1Kx6 1Kx8 1Kx12 1Kx19
+constexpr int kFillBf16Bwd[kNumResident] = {27,   27,   27,   32,   29,   29,   27,  27,  29,   27};
+constexpr int kFillBf16Fwd[kNumResident] = {30,   30,   30,   32,   32,   32,   32,  32,  30,   30};
+constexpr int kFillF32Bwd[kNumResident] = {27,    27,   27,   30,   30,   30,   27,  27,  27,   25};
+constexpr int kFillF32Fwd[kNumResident] = {27,    27,   27,   32,   32,   32,   27,  27,  27,   32};
+// Measured: bf16 backward from 256 x 4 up; bf16 forward all but 256 x 2; fp32 backward
+// 512 x 4, 512 x 8 and 1024 x 19; fp32 forward 512 x 4 and 1024 x 19. fp32 1024 x 6 .. 12
+// run one workgroup per row (kF32Persistent), so their fill is unused.
+constexpr int kFillF32Prefix = 32;
+constexpr int kFillBf16Prefix = 31;
 
 const void* pick_bf16_fwd(int i) {
   switch (i) {
@@ -1238,6 +1256,8 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
     L.two_buffers = dtype == DPPO_BF16 && bwd && kResidentDB[pick];
     L.resident = true;
     L.persistent = dtype == DPPO_BF16 || kF32Persistent[pick];
+    L.fill = dtype == DPPO_BF16 ? (bwd ? kFillBf16Bwd[pick] : kFillBf16Fwd[pick])
+                                : (bwd ? kFillF32Bwd[pick] : kFillF32Fwd[pick]);
     return L;
   }
   L.threads = 1024;
@@ -1250,6 +1270,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
     L.chunks = kPrefixNC;
     L.prefix = true;
     L.persistent = true;
+    L.fill = dtype == DPPO_F32 ? kFillF32Prefix : kFillBf16Prefix;
     return L;
   }
   if (dtype == DPPO_BF16) {

@@ -269,6 +269,8 @@ hipError_t launch_shard_combine(const float* lse_s, int32_t P, int64_t T, float*
   return hipGetLastError();
 }
 
+constexpr int kShardLossFill = 27;  // CUs used per 32
+
 hipError_t launch_shard_loss(const ShardArgs& s, bool bf16, bool vec, hipStream_t st) {
   const void* fn = bf16 ? (vec ? (const void*)shard_loss<true, true> : (const void*)shard_loss<true, false>)
                         : (vec ? (const void*)shard_loss<false, true> : (const void*)shard_loss<false, false>);
@@ -280,7 +282,7 @@ hipError_t launch_shard_loss(const ShardArgs& s, bool bf16, bool vec, hipStream_
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kNT, 0);
   if (e != hipSuccess) return e;
-  const int64_t used_cus = cus * 27 / 32 > 0 ? cus * 27 / 32 : 1;
+  const int64_t used_cus = cus * kShardLossFill / 32 > 0 ? cus * kShardLossFill / 32 : 1;
   const int64_t slots = used_cus * (per_cu >= 2 ? 2 : (per_cu > 0 ? per_cu : 1));
   const unsigned grid = (unsigned)(s.a.T < slots ? s.a.T : slots);
   void* args[] = {const_cast<ShardArgs*>(&s)};
