@@ -115,10 +115,12 @@ dppo_status launch_rows(const dppo::RowLaunch& L, const dppo::RowArgsV& args, in
     if (slots < 1) slots = 1;
     if (slots < grid) grid = slots;
   }
+  dppo::RowArgsV a = args;
+  a.stagger = L.stagger;
   auto* ev = timer_slot();
   if (ev) (void)hipEventRecord(ev->first, st);
   // Gradient kernels take the RowArgs part alone, the others the whole RowArgsV.
-  const void* karg = L.bwd ? (const void*)static_cast<const dppo::RowArgs*>(&args) : (const void*)&args;
+  const void* karg = L.bwd ? (const void*)static_cast<const dppo::RowArgs*>(&a) : (const void*)&a;
   void* kargs[] = {const_cast<void*>(karg)};
   hipError_t e = hipLaunchKernel((const void*)L.fn, dim3((unsigned)grid), dim3((unsigned)L.threads),
                                  kargs, 0, st);

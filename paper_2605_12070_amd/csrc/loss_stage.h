@@ -43,6 +43,8 @@ struct RowArgs {
   int32_t scale_mode;
   int32_t ref_mode;     // dppo_ref_mode; lp_ref is NULL unless GIVEN
   float alpha;          // behaviour-policy weight of an interpolated reference
+  int32_t stagger;      // persistent bf16 kernels: start delay per XCD-local workgroup index,
+                        // in s_sleep(6) units (set by the launcher from RowLaunch)
 };
 
 // Arguments of the kernels without the backward sweep: the row arguments plus an optional
@@ -67,6 +69,7 @@ struct RowLaunch {
   bool two_buffers = false; // resident backward kernel with two row buffers
   bool prefix = false;       // backward kernel with a resident prefix and a streamed tail
   int fill = 27;             // persistent grids: workgroups launched per 32 resident slots
+  int stagger = 2;           // RowArgs::stagger for the kernels that stagger their starts
 };
 
 constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the prefix kernels

@@ -172,11 +172,11 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   // Stagger the start of the workgroups that share an XCD: workgroups are dealt to the
   // eight XCDs in turn, so blockIdx / 8 numbers them within their XCD. Started together,
   // they would load, compute and store in lockstep and leave the XCD's memory path idle
-  // while they all compute; offsets of up to a third of a row's time keep it busy (about
-  // 1 % faster on MI355X). The host launches 27 workgroups per 32 CUs (see the ABI layer).
+  // while they all compute; offsets of up to a third of a row's time keep it busy (1-4 %
+  // faster on MI355X, the offset chosen per shape by the launcher).
   if (a.T >= 4 * (int64_t)gridDim.x) {
-    const int steps = (int)((blockIdx.x >> 3) & 31);
-    for (int i = 0; i < steps; ++i) __builtin_amdgcn_s_sleep(12);
+    const int steps = (int)((blockIdx.x >> 3) & 31) * a.stagger;
+    for (int i = 0; i < steps; ++i) __builtin_amdgcn_s_sleep(6);
   }
   bool rd_cur = row < a.T && reads(row);
   {
@@ -396,8 +396,8 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
   StatCount sc;
   int64_t row = blockIdx.x;
   if (a.T >= 4 * (int64_t)gridDim.x) {      // staggered starts, as in rows_bf16_resident
-    const int steps = (int)((blockIdx.x >> 3) & 31);
-    for (int i = 0; i < steps; ++i) __builtin_amdgcn_s_sleep(12);
+    const int steps = (int)((blockIdx.x >> 3) & 31) * a.stagger;
+    for (int i = 0; i < steps; ++i) __builtin_amdgcn_s_sleep(6);
   }
   bool rd_cur = row < a.T && reads(row);
   {
@@ -1173,6 +1173,14 @@ constexpr int kFillF32Fwd[kNumResident] = {27,    27,   27,   32,   32,   32,   
 // run one workgroup per row (kF32Persistent), so their fill is unused.
 constexpr int kFillF32Prefix = 32;
 constexpr int kFillBf16Prefix = 31;
+// Start stagger of the persistent bf16 kernels (RowArgs::stagger: s_sleep(6) units per
+// XCD-local workgroup index, up to 31 indices): longer rows want longer offsets. Same-box
+// sweeps of 0 to 6: the flagship is fastest at 4 (0.5 % faster than 2), 512 x 4 backward and
+// 512 x 8 forward at 0 (4 %), the small_vocab shape (512 x 8 backward, T = 4096) at 1 (1 %);
+// 1024 x 8 and 1024 x 12 backward are flat from 1 to 4.
+// Shapes:                                   256x1 256x2 256x4 512x4 512x6 512x8 1Kx6 1Kx8 1Kx12 1Kx19
+constexpr int kStagBf16Bwd[kNumResident] = {0,    0,    0,    0,    1,    1,    2,   2,   2,    4};
+constexpr int kStagBf16Fwd[kNumResident] = {0,    0,    0,    0,    0,    0,    1,   1,   2,    2};
 
 const void* pick_bf16_fwd(int i) {
   switch (i) {
@@ -1258,6 +1266,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
     L.persistent = dtype == DPPO_BF16 || kF32Persistent[pick];
     L.fill = dtype == DPPO_BF16 ? (bwd ? kFillBf16Bwd[pick] : kFillBf16Fwd[pick])
                                 : (bwd ? kFillF32Bwd[pick] : kFillF32Fwd[pick]);
+    L.stagger = dtype == DPPO_BF16 ? (bwd ? kStagBf16Bwd[pick] : kStagBf16Fwd[pick]) : 0;
     return L;
   }
   L.threads = 1024;
