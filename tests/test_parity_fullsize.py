@@ -173,3 +173,51 @@ def test_versioned_logprob_fullsize():
                                    wl.ids[idx].cpu().numpy())
     err = np.abs(got[rows] - ref) / np.maximum(np.abs(ref), 1.0)
     assert err.max() < 2e-5, err.max()
+
+
+def test_fp32_long_rows_fullsize():
+    """fp32 rows at the benchmark's fp32 size (T = 8192, V = 151936): the resident-prefix
+    kernel on its persistent grid (several rows per workgroup), fp32 logits ~ N(0, 2^2) with
+    the tiny workload's recipe, sampled rows against the oracle and the row properties on
+    every row."""
+    wl = W.make_workload("tiny", device=DEV, T=8192, V=151936, seed=13, seq_len=32)
+    assert wl.logits.dtype == torch.float32
+    assert P.row_kernel_name(torch.float32, wl.V) == "dppo::rows_f32_prefix<1024, 19>"
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    _check_workload(wl, lp_ref, lp_mu, lp_ref.cpu().double().numpy())
+
+
+def test_small_vocab_fullsize_every_row():
+    """The small-vocabulary workload at its benchmark size (T = 4096, V = 32000, bf16, 1 % of
+    rows with a spiked logit, 5 % of tokens pushed out of the band): the two-buffer 512 x 8
+    kernel on its persistent grid, every row of lp, loss_tok, flags and dlogits against the
+    oracle, in blocks of rows."""
+    wl = W.make_workload("small_vocab", device=DEV)
+    T, V = wl.T, wl.V
+    assert (T, V) == (4096, 32000)
+    assert P.row_kernel_name(torch.bfloat16, V) == "dppo::rows_bf16_resident_db<512, 8>"
+    print(f"[case] fullsize small_vocab T={T} V={V}", flush=True)
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    res = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask)
+    torch.cuda.synchronize()
+    m = wl.mask.cpu().numpy()
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
+    scale = oracle.batch_scale(m, params)
+    ids_np = wl.ids.cpu().numpy()
+    for a in range(0, T, 512):
+        rows = np.arange(a, min(T, a + 512))
+        idx = torch.as_tensor(rows, device=DEV)
+        ref = oracle.per_token(bits_of(wl.logits[idx]), ids_np[rows],
+                               lp_mu[idx].cpu().double().numpy(),
+                               lp_ref[idx].cpu().double().numpy(),
+                               wl.adv[idx].cpu().double().numpy(), m[rows], None, params, scale)
+        compare_loss(res, ref, params, torch.bfloat16, rows=rows)
+    fl = res.flags.cpu().numpy()
+    st = res.stats.cpu().numpy()
+    np.testing.assert_array_equal(st, oracle.stats_of(fl, params))
+    assert st[0] == T and st[0] - st[1] > 0.03 * T        # the pushed tokens leave the band
+    lt = res.loss_tok.cpu().double().numpy()
+    own = float(np.sum(scale * lt))
+    assert abs(res.loss.item() - own) <= 1e-6 * (np.sum(np.abs(scale * lt)) + 1e-30)

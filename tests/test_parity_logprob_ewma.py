@@ -178,3 +178,40 @@ def test_logprob_versioned(dtype, V, K, policy):
     ok = ~np.isnan(ref)
     err = np.abs(got[ok] - ref[ok]) / np.maximum(np.abs(ref[ok]), 1.0)
     assert err.max() < 2e-5, err.max()
+
+
+def test_ewma_parameter_sized_buffer():
+    """The PPO-EWMA update at the benchmark's parameter-sized shape (n = 2^30 fp32, normalised
+    form): the first step copies, the second and third follow the recursion of App. B.
+    Sampled elements (2^20 random ones plus both ends) are compared with the oracle's
+    recursion; on every element, the result lies between the old value and the new one
+    (a convex combination), which any misplaced read or write would break."""
+    n = 1 << 30
+    print(f"[case] ewma parameter-sized n={n}", flush=True)
+    g = torch.Generator(device=DEV).manual_seed(30)
+    hist = [torch.randn(n, generator=g, device=DEV) for _ in range(3)]
+    x = torch.empty(n, device=DEV)
+    beta = P.beta_from_window(6)
+    rng = np.random.default_rng(30)
+    idx = np.unique(np.concatenate([rng.integers(0, n, 1 << 20), [0, 1, n - 2, n - 1]]))
+    it = torch.as_tensor(idx, device=DEV)
+    w, w_ref, x_ref = 0.0, 0.0, None
+    for t, th in enumerate(hist):
+        prev = x.clone() if t > 0 else None
+        w = P.ewma_proxy_update(x, th, beta, w)
+        x_ref, w_ref = oracle.ewma_normalized_step(x_ref, th[it].cpu().double().numpy(), beta,
+                                                   w_ref)
+        torch.cuda.synchronize()
+        assert abs(w - w_ref) < 1e-12
+        np.testing.assert_allclose(x[it].cpu().double().numpy(), x_ref, rtol=2e-6 * (t + 1),
+                                   atol=2e-6 * (t + 1))
+        if prev is None:
+            assert torch.equal(x, th)
+        else:
+            for a in range(0, n, 1 << 28):
+                lo = torch.minimum(prev[a:a + (1 << 28)], th[a:a + (1 << 28)])
+                hi = torch.maximum(prev[a:a + (1 << 28)], th[a:a + (1 << 28)])
+                xs = x[a:a + (1 << 28)]
+                slack = 1e-6 * torch.maximum(lo.abs(), hi.abs())
+                assert torch.all((xs >= lo - slack) & (xs <= hi + slack))
+            del prev
