@@ -142,7 +142,7 @@ dppo_status check_matrix(const void* p, int32_t dtype, int64_t T, int64_t V, int
 }
 
 struct LmhLayout {
-  int64_t part, zy, w, lse2, ev, g, total;  // byte offsets into the workspace, and its size
+  int64_t part, zy, w, lse2, dy, ev, g, total;  // byte offsets into the workspace, and its size
   int64_t chunk, ldg;                        // vocabulary rows per backward chunk, g's stride
   bool one_pass;                             // G from the forward tiles' exponentials
 };
@@ -167,6 +167,7 @@ LmhLayout lmh_layout(int64_t T, int64_t V, int64_t vocab_chunk) {
   L.zy = o;   o = align256(o + T * 4);
   L.w = o;    o = align256(o + T * 4);
   L.lse2 = o; o = align256(o + T * 4);
+  L.dy = o;   o = align256(o + T * 4);
   L.ev = o;   o = align256(o + T);
   L.g = o;    o = align256(o + T * L.ldg * 2);
   L.total = o;
@@ -523,6 +524,7 @@ dppo_status fused_lm_head_loss_fwd_bwd(
     m.zy = (float*)(ws + L.zy);
     m.w = (float*)(ws + L.w);
     m.lse2 = (float*)(ws + L.lse2);
+    m.dy = (float*)(ws + L.dy);
     m.ev = (uint8_t*)(ws + L.ev);
     m.ids = token_ids;
     m.g = (uint16_t*)(ws + L.g);
@@ -603,7 +605,7 @@ dppo_status fused_lm_head_loss_fwd_bwd(
     if ((e = timed([&] { return dppo::launch_lmh_fwd_tiles(m, st); })) != hipSuccess)
       return hip_fail(e, "forward tile launch");
     if (m.store_p) {
-      // one pass: the row pass finishes every token and forms G in place
+      // one pass: the row pass finishes every token, the scale pass forms G in place
       if ((e = dppo::launch_lmh_grad_rows(a, m, st)) != hipSuccess) return hip_fail(e, "gradient row launch");
       s = products(0, V);
       if (s != DPPO_OK) return s;

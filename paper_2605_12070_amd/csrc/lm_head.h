@@ -35,6 +35,7 @@ struct LmhArgs {
   float* zy;               // z[t, y_t] (dot-product kernel)
   float* w;                // MIS weight per token (0 where the gradient is zero)
   float* lse2;             // log2 sum_v 2^(z log2 e) per token
+  float* dy;               // w (p_y - 1) per token: the sampled entry of G (one pass)
   uint8_t* ev;             // 1 where the token was evaluated (valid row, good id)
   const int64_t* ids;
   uint16_t* g;             // [T, ldg]: the forward tiles' fp16 exponentials 2^(z log2 e - m2)

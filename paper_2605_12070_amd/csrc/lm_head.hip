@@ -4,10 +4,10 @@
 //                  log-sum-exps of each 128-entry vocabulary group; optionally also stores
 //                  the group-normalised exponentials 2^(z log2 e - m2) as fp16;
 //   lmh_zy         z[t, y_t] as one dot product per token;
-//   lmh_grad_rows  per token row: merges the partials into lse_t, runs the token math of
-//                  Eq. 1-4 (ratios, band, PPO clip, loss, MIS weight w_t) and turns the
-//                  row's stored exponentials into G = w_t (softmax - onehot) in bf16, the
-//                  operand of the two gradient products (lm_head_grad.hip);
+//   lmh_row_stats  per token row: merges the partials into lse_t and runs the token math
+//                  of Eq. 1-4 (ratios, band, PPO clip, loss, MIS weight w_t);
+//   lmh_grad_scale turns the stored exponentials into G = w_t (softmax - onehot) in bf16,
+//                  the operand of the two gradient products (lm_head_grad.hip);
 //   lmh_finish     the same merge and token math without G (forward only, or the
 //                  vocabulary-chunk mode);
 //   lmh_bwd_tiles  vocabulary-chunk mode: recomputes a tile and writes G for one chunk.
@@ -390,92 +390,92 @@ __global__ __launch_bounds__(256) void lmh_finish(RowArgs a, LmhArgs m) {
   }
 }
 
-// Full-vocabulary backward without a second product: one workgroup per token row, looping
-// over rows. Merges the row's group partials into lse2, runs the token math (per-token
-// outputs, counters kept per workgroup), then turns the row's stored exponentials into
-// G = w (softmax - onehot) in place: entry v of group q becomes w 2^(m2_q - lse2) e_v in
-// bf16, the sampled entry w (p_y - 1) as token_math computes it from z[y], and the entries
-// from V up to ldg become zeros. A row that is not evaluated (masked, or a bad id) becomes
-// zeros. Four 16-byte chunks per thread are in flight at a time.
+// Full-vocabulary backward without a second product, in two passes.
+// lmh_row_stats, one 256-thread workgroup per token row (looping over rows): merges the
+// row's group partials into lse2, runs the token math (per-token outputs, counters kept per
+// workgroup) and leaves the backward constants w, lse2, dy = w (p_y - 1) (as token_math
+// computes it from z[y]) and ev for the scale pass.
+// lmh_grad_scale turns the stored exponentials into G = w (softmax - onehot) in place, one
+// 16-byte chunk (8 entries) per thread: entry v of group q becomes w 2^(m2_q - lse2) e_v in
+// bf16, the sampled entry dy, and the entries from V up to ldg zeros; a row that is not
+// evaluated (masked, or a bad id) becomes zeros without being read. One chunk per thread
+// and a grid of (chunks per row / 256) x T workgroups is the shape in which a read-write
+// stream moves the most bytes per second on MI355X (as a per-row loop over four chunks per
+// thread it took 1.0 ms at T = 8192, V = 151936).
 constexpr int kGR = 256;
 
-__global__ __launch_bounds__(kGR) void lmh_grad_rows(RowArgs a, LmhArgs m) {
+__global__ __launch_bounds__(kGR) void lmh_row_stats(RowArgs a, LmhArgs m) {
   __shared__ float red[2 * (kGR / 64) + 2];
-  __shared__ float bc[2];
   StatCount sc;
   const int tid = threadIdx.x;
   const int ngroups = lmh_groups(m.V);
-  const int nchunk = (int)(m.ldg / 8);
   for (int64_t row = blockIdx.x; row < m.T; row += gridDim.x) {
     const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
     const int64_t y = uload(m.ids + row);
     const bool ev = valid && y >= 0 && y < m.V;           // uniform over the workgroup
-    float w = 0.0f, l2 = 0.0f, dy = 0.0f;
     if (ev) {
       float n = -INFINITY, s = 0.0f;
       for (int q = tid; q < ngroups; q += kGR) {
         const float* p = m.part + (row * ngroups + q) * 2;
         merge_ns(n, s, p[0], p[1]);
       }
-      block_merge_ns<kGR>(n, s, red);
-      l2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+      block_merge_ns<kGR>(n, s, red);  // once per row: its second barrier orders the reuse
+      const float l2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
       if (tid == 0) {
         const TokenOut o = token_math(a, token_inputs(a, row), uload(m.zy + row), l2);
         a.lp_out[row] = o.lp;
         a.loss_tok[row] = o.loss;
         if (a.flags) a.flags[row] = o.flags;
         count_stats(a, o.flags, sc);
-        bc[0] = o.w;
-        bc[1] = o.dy;
+        m.w[row] = o.w;
+        m.lse2[row] = l2;
+        m.dy[row] = o.dy;
+        m.ev[row] = 1;
       }
-      __syncthreads();
-      w = bc[0];
-      dy = bc[1];
     } else if (tid == 0) {
       a.lp_out[row] = valid ? __builtin_nanf("") : 0.0f;
       a.loss_tok[row] = 0.0f;
       if (a.flags) a.flags[row] = valid ? (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID) : (uint8_t)0;
       if (valid) sc.bad += 1;
-    }
-    uint16_t* grow = m.g + row * m.ldg;
-    const float* prt = m.part + row * ngroups * 2;
-    for (int c0 = tid; c0 < nchunk; c0 += 4 * kGR) {
-      u32x4 e[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = c0 + k * kGR;
-        e[k] = (ev && c < nchunk && 8 * c < m.V)
-                   ? __builtin_nontemporal_load((const u32x4*)(grow + 8 * c))
-                   : u32x4{0u, 0u, 0u, 0u};
-      }
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = c0 + k * kGR;
-        if (c >= nchunk) break;
-        const int v0 = 8 * c;
-        u32x4 out = {0u, 0u, 0u, 0u};
-        if (ev && v0 < m.V) {
-          const float m2 = prt[(v0 / LMH_GROUP) * 2];
-          const float f = w * exp2_hw(m2 - l2);
-          float x[8];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            x[2 * j] = f16_lo_mul(e[k][j], f);
-            x[2 * j + 1] = f16_hi_mul(e[k][j], f);
-          }
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            if ((int64_t)(v0 + j) == y) x[j] = dy;
-            if (v0 + j >= m.V) x[j] = 0.0f;
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j) out[j] = pack_bf16(x[2 * j], x[2 * j + 1]);
-        }
-        __builtin_nontemporal_store(out, (u32x4*)(grow + v0));
-      }
+      m.w[row] = 0.0f;
+      m.lse2[row] = 0.0f;
+      m.dy[row] = 0.0f;
+      m.ev[row] = 0;
     }
   }
   if (tid == 0) flush_stats(a, sc);
+}
+
+__global__ __launch_bounds__(256) void lmh_grad_scale(LmhArgs m, int per_row) {
+  // per_row workgroups cover a row's chunks; consecutive workgroups walk along a row
+  const int64_t row = blockIdx.x / per_row;
+  const int c = (int)(blockIdx.x % per_row) * 256 + threadIdx.x;
+  if (c >= (int)(m.ldg / 8)) return;
+  const int v0 = 8 * c;
+  uint16_t* grow = m.g + row * m.ldg;
+  const bool ev = uload_u8(m.ev + row) != 0;              // uniform over the workgroup
+  u32x4 out = {0u, 0u, 0u, 0u};
+  if (ev && v0 < m.V) {
+    const u32x4 e = __builtin_nontemporal_load((const u32x4*)(grow + v0));
+    const float w = uload(m.w + row), l2 = uload(m.lse2 + row), dy = uload(m.dy + row);
+    const int64_t y = uload(m.ids + row);
+    const float m2 = m.part[(row * lmh_groups(m.V) + v0 / LMH_GROUP) * 2];
+    const float f = w * exp2_hw(m2 - l2);
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[2 * j] = f16_lo_mul(e[j], f);
+      x[2 * j + 1] = f16_hi_mul(e[j], f);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if ((int64_t)(v0 + j) == y) x[j] = dy;
+      if (v0 + j >= m.V) x[j] = 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[j] = pack_bf16(x[2 * j], x[2 * j + 1]);
+  }
+  __builtin_nontemporal_store(out, (u32x4*)(grow + v0));
 }
 
 // Backward (vocabulary chunks): g[t, v - n0] = w_t (softmax(z_t)[v] - 1{v = y_t}) in bf16
@@ -542,9 +542,15 @@ hipError_t launch_lmh_finish(const RowArgs& a, const LmhArgs& m, hipStream_t st)
 }
 
 hipError_t launch_lmh_grad_rows(const RowArgs& a, const LmhArgs& m, hipStream_t st) {
-  if (m.ldg % 8 != 0) return hipErrorInvalidValue;
+  if (m.ldg % 8 != 0 || m.ldg / 8 > 0x7fffffff) return hipErrorInvalidValue;
+  if (m.T <= 0) return hipSuccess;
   const int grid = m.T < 2048 ? m.T : 2048;
-  if (grid > 0) lmh_grad_rows<<<grid, kGR, 0, st>>>(a, m);
+  lmh_row_stats<<<grid, kGR, 0, st>>>(a, m);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t per_row = (m.ldg / 8 + 255) / 256;
+  if (per_row * m.T > 0x7fffffff) return hipErrorInvalidValue;
+  lmh_grad_scale<<<(unsigned)(per_row * m.T), 256, 0, st>>>(m, (int)per_row);
   return hipGetLastError();
 }
 
