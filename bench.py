@@ -244,7 +244,8 @@ def vocab_shard_measure(dev, wl, lp_mu, lp_ref, n_shards=8, reps=20):
     ach = b_loss / (k_loss * 1e-3) / 1e9
     del shard, dl
     return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(ach / HBM_PEAK_GBPS, 4), "kernel": "dppo::shard_loss<true, true>",
+            "frac": round(ach / HBM_PEAK_GBPS, 4),
+            "kernel": "dppo::shard_token + dppo::shard_grad<true> (the shard loss call)",
             "kernel_ms": round(k_loss, 4), "alg_bytes_per_launch": b_loss,
             "traffic": recorded_traffic("vocab_shard_loss", SHARD_SOURCES),
             "shard": f"T={T} x Vs={Vs} (V/{n_shards}) bf16, contiguous",

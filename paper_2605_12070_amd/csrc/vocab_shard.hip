@@ -271,7 +271,139 @@ hipError_t launch_shard_combine(const float* lse_s, int32_t P, int64_t T, float*
 
 constexpr int kShardLossFill = 27;  // CUs used per 32
 
+// The shard loss on aligned rows as two kernels instead of shard_loss:
+//   shard_token  one thread per token: the token math from the global lse and z[y], the
+//                per-token outputs, and the counters (one add per workgroup);
+//   shard_grad   one 16-byte chunk of dlogits per thread, (chunks per row / kGradNT) workgroups
+//                per row: thread 0 repeats the row's token math for w, lse2 and dy (the same
+//                operations on the same inputs, so the same values), the workgroup shares
+//                them through LDS, and every thread writes w 2^(z log2 e - lse2) for its
+//                chunk; the thread whose chunk holds the sampled column then writes dy there.
+//                A row that is not evaluated is written as zeros without being read.
+// One chunk per thread over many small workgroups is the shape in which a read-write stream
+// moves the most bytes per second on MI355X.
+__global__ __launch_bounds__(256) void shard_token(ShardArgs s) {
+  const RowArgs& a = s.a;
+  const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool uses_mask = a.rd_mode == DPPO_RD_MASK || a.rd_mode == DPPO_RD_MASK_WEIGHT;
+  bool band = false, ppo = false, active = false, bad = false;
+  if (row < a.T) {
+    const bool valid = a.mask == nullptr || a.mask[row] != 0;
+    const int64_t y = a.ids[row];
+    const bool ev = valid && y >= 0 && y < s.vtot;
+    if (!valid) {
+      a.lp_out[row] = 0.0f;
+      a.loss_tok[row] = 0.0f;
+      if (a.flags) a.flags[row] = 0;
+    } else if (!ev) {
+      a.lp_out[row] = __builtin_nanf("");
+      a.loss_tok[row] = 0.0f;
+      if (a.flags) a.flags[row] = (uint8_t)(DPPO_FLAG_VALID | DPPO_FLAG_BAD_ID);
+      bad = true;
+    } else {
+      const float lse2 = s.lse_in[row] * kLog2e;
+      const TokenOut o = token_math(a, token_inputs_lane(a, row), s.zy_in[row], lse2);
+      a.lp_out[row] = o.lp;
+      a.loss_tok[row] = o.loss;
+      if (a.flags) a.flags[row] = o.flags;
+      band = o.flags & DPPO_FLAG_BAND;
+      ppo = o.flags & DPPO_FLAG_PPO;
+      active = ppo && (band || !uses_mask);
+    }
+  }
+  const int nb = __syncthreads_count(band);
+  const int np = __syncthreads_count(ppo);
+  const int na = __syncthreads_count(active);
+  const int nbad = __syncthreads_count(bad);
+  if (threadIdx.x == 0) {
+    if (nb) atomicAdd(&a.stats[DPPO_STAT_N_BAND], nb);
+    if (np) atomicAdd(&a.stats[DPPO_STAT_N_PPO], np);
+    if (na) atomicAdd(&a.stats[DPPO_STAT_N_ACTIVE], na);
+    if (nbad) atomicAdd(&a.stats[DPPO_STAT_N_BAD], nbad);
+  }
+}
+
+constexpr int kGradNT = 512;  // threads of a shard_grad workgroup (128-1024 measured)
+
+template <bool BF16>
+__global__ __launch_bounds__(kGradNT) void shard_grad(ShardArgs s, int per_row) {
+  __shared__ float rb[4];
+  const RowArgs& a = s.a;
+  constexpr int ES = BF16 ? 2 : 4;
+  constexpr int E = 16 / ES;
+  const int64_t row = blockIdx.x / per_row;
+  const int c = (int)(blockIdx.x % per_row) * kGradNT + threadIdx.x;
+  const int Vs = a.V;
+  const int nfull = Vs / E;
+  const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
+  const int64_t y = uload(a.ids + row);
+  const bool ev = valid && y >= 0 && y < s.vtot;          // uniform over the workgroup
+  const char* zp = (const char*)a.logits + row * a.ld * ES;
+  char* dp = (char*)a.dlogits + row * a.ldd * ES;
+  const __amdgpu_buffer_rsrc_t rz = row_rsrc(zp, ev ? nfull * 16 : 0);
+  const __amdgpu_buffer_rsrc_t rd = row_rsrc(dp, nfull * 16);
+  const u32x4 v = buf_load16<kAuxLast>(rz, c * 16, 0);     // past the row or not read: zeros
+  if (ev && threadIdx.x == 0) {
+    const float lse2 = uload(s.lse_in + row) * kLog2e;
+    const TokenOut o = token_math(a, token_inputs(a, row), uload(s.zy_in + row), lse2);
+    rb[0] = o.w;
+    rb[1] = lse2;
+    rb[2] = o.dy;
+  }
+  __syncthreads();
+  const float w = ev ? rb[0] : 0.0f, lse2 = ev ? rb[1] : 0.0f;
+  float x[E];
+  unpack<BF16>(v, x);
+  u32x4 o;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (BF16) {
+      o[k] = pack_bf16(ev ? w * exp2_hw(__builtin_fmaf(x[2 * k], kLog2e, -lse2)) : 0.0f,
+                       ev ? w * exp2_hw(__builtin_fmaf(x[2 * k + 1], kLog2e, -lse2)) : 0.0f);
+    } else {
+      o[k] = __float_as_uint(ev ? w * exp2_hw(__builtin_fmaf(x[k], kLog2e, -lse2)) : 0.0f);
+    }
+  }
+  buf_store16_nt(o, rd, c * 16, 0);                        // past the row: dropped
+  // the V % E last entries of the row, by the thread after the last whole chunk
+  if (c == nfull) {
+    for (int i = nfull * E; i < Vs; ++i) {
+      const float g = ev ? w * exp2_hw(__builtin_fmaf(elem<BF16>(zp, i), kLog2e, -lse2)) : 0.0f;
+      if (BF16) ((uint16_t*)dp)[i] = to_bf16(g);
+      else ((float*)dp)[i] = g;
+    }
+  }
+  // the sampled column, when this shard holds it, by the thread that wrote its entry
+  const int64_t yl = y - s.vstart;
+  if (ev && yl >= 0 && yl < Vs && c == (yl < (int64_t)nfull * E ? (int)(yl / E) : nfull)) {
+    const float dy = rb[2];
+    if (yl < (int64_t)nfull * E) {
+      if (BF16) __builtin_amdgcn_raw_buffer_store_b16(to_bf16(dy), rd, (int)(yl * 2), 0, kAuxNT);
+      else __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(dy), rd, (int)(yl * 4), 0, kAuxNT);
+    } else if (BF16) {
+      ((uint16_t*)dp)[yl] = to_bf16(dy);
+    } else {
+      ((float*)dp)[yl] = dy;
+    }
+  }
+}
+
+constexpr bool kShardFlat = true;  // aligned rows with dlogits: shard_token + shard_grad
+
 hipError_t launch_shard_loss(const ShardArgs& s, bool bf16, bool vec, hipStream_t st) {
+  if (kShardFlat && vec && s.a.dlogits != nullptr) {
+    if (s.a.T <= 0) return hipSuccess;
+    shard_token<<<(unsigned)((s.a.T + 255) / 256), 256, 0, st>>>(s);
+    const hipError_t e0 = hipGetLastError();
+    if (e0 != hipSuccess) return e0;
+    const int E = bf16 ? 8 : 4;
+    const int64_t per_row = (s.a.V / E + kGradNT) / kGradNT;  // whole chunks, the tail thread
+    if (per_row * s.a.T > 0x7fffffff) return hipErrorInvalidValue;
+    const unsigned grid = (unsigned)(per_row * s.a.T);
+    if (bf16) shard_grad<true><<<grid, kGradNT, 0, st>>>(s, (int)per_row);
+    else shard_grad<false><<<grid, kGradNT, 0, st>>>(s, (int)per_row);
+    return hipGetLastError();
+  }
   const void* fn = bf16 ? (vec ? (const void*)shard_loss<true, true> : (const void*)shard_loss<true, false>)
                         : (vec ? (const void*)shard_loss<false, true> : (const void*)shard_loss<false, false>);
   // Persistent grid: two workgroups on 27 of every 32 CUs, each looping over rows. At

@@ -197,3 +197,44 @@ def test_shard_pipeline_full_size():
         s, mag = d.sum(dim=1).abs(), d.abs().sum(dim=1)
         assert bool((s <= (2.0 ** -8 + 1e-5) * mag + 1e-7).all()), f"row sums, rows {a}.."
     del d_full
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_shard_ragged_tail_holds_the_sampled_column(dtype):
+    """An aligned shard whose width is not a whole number of 16-byte chunks (columns
+    [0, 1003) of a 1024-column row): the last entries are written by the thread after the
+    last whole chunk. Sampled columns are put in that tail, in the last whole chunk, in the
+    first column and outside the shard, on valid, masked and bad-id rows."""
+    T, V, cuts = 96, 1024, (0, 1003, 1024)
+    _say("vocab shard ragged tail", dtype)
+    g = torch.Generator(device=DEV).manual_seed(17)
+    logits = (torch.randn(T, V, generator=g, device=DEV) * 3).to(dtype)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    picks = [1000, 1001, 1002, 999, 992, 0, 1003, 1023]
+    for i in range(T):
+        ids[i] = picks[i % len(picks)] if i % 3 else ids[i]
+    ids[5] = V + 1
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    mask[9::11] = 0
+    anchor = torch_anchor(logits, ids.clamp(0, V - 1))
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.05 * torch.randn(T, generator=g, device=DEV,
+                                                  dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    kw = dict(scale_mode="const", loss_scale=1.0)
+    d_full = torch.full_like(logits, float("nan"))
+    _, lse, zy, outs = _gpu_pipeline(logits, ids, mask, lp_mu, lp_ref, adv, cuts, kw,
+                                     dlogits_full=d_full)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    z, idn, mk = bits_of(logits), ids.cpu().numpy(), mask.cpu().numpy()
+    scale = oracle.batch_scale(mk, params)
+    for (a, b), out in zip(zip(cuts, cuts[1:]), outs):
+        ref = oracle.vocab_shard_loss(z[:, a:b], idn, a, V, lse.cpu().double().numpy(),
+                                      zy.cpu().double().numpy(), lp_mu.cpu().double().numpy(),
+                                      lp_ref.cpu().double().numpy(), adv.cpu().double().numpy(),
+                                      mk, None, params, scale)
+        ties = tie_mask(ref, params)
+        rows = np.nonzero(~ties)[0]
+        check_dlogits_rows(bits_of(d_full[:, a:b])[rows], ref["dlogits"][rows], ref["w"][rows],
+                           dtype)
+    assert not torch.isnan(d_full.float()).any(), "every entry of every shard is written"
