@@ -388,7 +388,11 @@ dppo_status logprob_fwd_versioned(const void* const* logits, int32_t K, int32_t 
   const int es = esize_of(dtype);
   bool aligned = (ld * es) % 16 == 0;
   for (int v = 0; v < K; ++v) aligned = aligned && aligned16(logits[v]);
-  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
+  dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
+  // Rows gathered from several versions' logits want every slot of the device: at
+  // 1024 x 19 (bf16, V = 151936, 4 versions) 32 of 32 slots took 0.753-0.757 ms against
+  // 0.762-0.768 ms with the 30 that suit one matrix (same-box sweep).
+  if (K > 1 && dtype == DPPO_BF16 && L.resident && L.threads == 1024 && L.chunks == 19) L.fill = 32;
   dppo::RowArgsV a{};
   a.logits = logits[0];
   a.version = version_ids;
