@@ -6,10 +6,11 @@
 //   shard_stats  per row: log-sum-exp over the shard's columns, and z[y] when the shard
 //                holds column y (0 otherwise);
 //   shard_combine  lse = log sum_s exp(lse_s) over the gathered shard statistics;
-//   shard_loss   per row: the token math of Eq. 1-4 from the global lse and z[y] (every
-//                shard computes the same per-token values), then this shard's columns of
+//   shard_token, shard_grad (aligned rows with dlogits) or shard_loss (otherwise): the
+//                token math of Eq. 1-4 from the global lse and z[y] (every shard computes
+//                the same per-token values), then this shard's columns of
 //                dlogits = w (softmax - onehot).
-// One workgroup of 256 threads per row; 16-byte vector accesses on aligned rows.
+// 16-byte vector accesses on aligned rows.
 #include "dppo.h"
 #include "dppo_device.h"
 #include "loss_stage.h"
@@ -388,10 +389,9 @@ __global__ __launch_bounds__(kGradNT) void shard_grad(ShardArgs s, int per_row) 
   }
 }
 
-constexpr bool kShardFlat = true;  // aligned rows with dlogits: shard_token + shard_grad
 
 hipError_t launch_shard_loss(const ShardArgs& s, bool bf16, bool vec, hipStream_t st) {
-  if (kShardFlat && vec && s.a.dlogits != nullptr) {
+  if (vec && s.a.dlogits != nullptr) {                    // shard_token + shard_grad
     if (s.a.T <= 0) return hipSuccess;
     shard_token<<<(unsigned)((s.a.T + 255) / 256), 256, 0, st>>>(s);
     const hipError_t e0 = hipGetLastError();
