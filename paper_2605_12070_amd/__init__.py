@@ -21,13 +21,14 @@ from ._lib import (DppoError, FLAG_BAD_ID, FLAG_BAND, FLAG_PPO, FLAG_VALID,  # n
                    STAT_N_VALID)
 
 __all__ = [
-    "logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "ewma_proxy_update", "LossResult",
+    "logprob_fwd", "decoupled_ppo_loss_fwd_bwd", "decoupled_ppo_loss", "ewma_proxy_update",
+    "LossResult",
     "EwmaProxy", "beta_from_window", "train_infer_mask_value", "ppo_clip_ratio",
     "DecoupledPPOLoss", "DppoError", "set_path_policy", "KernelTimer", "row_kernel_name", "effective_thresholds",
     "fused_lm_head_loss_fwd_bwd", "LmHeadResult", "lm_head_workspace_bytes",
     "fused_lm_head_loss_fwd_bwd_noalloc",
     "logprob_fwd_versioned", "EwmaProxyDevice", "vocab_shard_stats", "vocab_shard_combine",
-    "decoupled_ppo_loss_shard_fwd_bwd",
+    "decoupled_ppo_loss_shard_fwd_bwd", "FusedLMHeadLoss",
 ]
 
 
@@ -161,6 +162,15 @@ def decoupled_ppo_loss_fwd_bwd(logits, token_ids, logp_mu_old, logp_ref, advanta
         out.stats.data_ptr(), _stream(dev))
     _lib.check(st, "decoupled_ppo_loss_fwd_bwd")
     return out
+
+
+def decoupled_ppo_loss(logits, y, lp_mu, lp_ref, adv, mask=None, band=(0.5, 2.0),
+                       eps=(0.2, 0.2), rd_mode="mask_weight", scale="token_mean"):
+    """The loss stage in the short form: returns (loss, lp, dlogits, stats), the scalar loss
+    as a 0-d tensor. Argument marshalling over decoupled_ppo_loss_fwd_bwd."""
+    r = decoupled_ppo_loss_fwd_bwd(logits, y, lp_mu, lp_ref, adv, mask, band=band, clip_eps=eps,
+                                   rd_mode=rd_mode, scale_mode=scale)
+    return r.loss[0], r.logp, r.dlogits, r.stats
 
 
 def vocab_shard_stats(logits_shard, token_ids, vocab_start: int, vocab_size: int,

@@ -541,3 +541,18 @@ def test_forward_only_kernel_matches_gradient_call(V):
     params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "token_mean", 1.0)
     ref = run_oracle(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask, None, params)
     compare_loss(both, ref, params, wl.logits.dtype)
+
+
+def test_short_form_matches_the_full_call():
+    """decoupled_ppo_loss(...) -> (loss, lp, dlogits, stats) returns the full call's outputs."""
+    wl = W.make_workload("small_vocab", device=DEV, T=300, seed=5)
+    anchor = oracle_anchor(wl.logits, wl.ids).to(DEV)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    loss, lp, d, st = P.decoupled_ppo_loss(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask,
+                                           band=(0.6, 1.8), eps=(0.1, 0.3), rd_mode="mask")
+    full = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv, wl.mask,
+                                        band=(0.6, 1.8), clip_eps=(0.1, 0.3), rd_mode="mask")
+    torch.cuda.synchronize()
+    assert loss.dim() == 0 and torch.equal(loss.view(1), full.loss)
+    assert torch.equal(lp, full.logp) and torch.equal(st, full.stats)
+    assert torch.equal(d.view(torch.int16), full.dlogits.view(torch.int16))
