@@ -23,9 +23,16 @@
  *  - A loss mask ([T] uint8, where a call takes one) is read in aligned 4-byte words, so
  *    its allocation must be readable up to the next 4-byte boundary past mask + T (true of
  *    any hipMalloc or PyTorch allocation); the bytes past mask + T are ignored.
- *  - Row strides (`ld`, `ld_dlogits`) are in elements. When a base pointer is not 16-byte
- *    aligned or a stride is not a multiple of 16 bytes, a slower element-wise path runs;
- *    this is not an error.
+ *  - Row strides (`ld`, `ld_dlogits`) are in elements. bf16 rows that do not start on a
+ *    16-byte boundary, or whose length is not a multiple of 8, are read as the aligned
+ *    16-byte chunks that cover them: the logits allocation must be readable from the 16-byte
+ *    boundary at or below the first row to the one after the last row (true of any
+ *    hipMalloc or PyTorch allocation, and of views into one); only the rows' own entries
+ *    are written. This needs dlogits (if any) at the logits' offset within 16 bytes on
+ *    every row (the same pointer residue mod 16 and strides that differ by a multiple of 8
+ *    entries, as in place or for a tensor of the logits' layout). Other layouts, fp32 rows
+ *    that are not aligned, and rows longer than the resident kernels hold take a slower
+ *    streaming path; none of this is an error.
  *  - Thread safety: calls may be issued from several host threads; the kernel timer
  *    (dppo_timer_*) is process-global and meant for one profiling thread.
  */

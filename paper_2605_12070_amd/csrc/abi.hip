@@ -262,12 +262,19 @@ dppo_status dppo_timer_read(double* total_ms, int64_t* launches) {
 const char* dppo_row_kernel_name(int32_t dtype, int64_t V, int64_t ld, int32_t with_dlogits) {
   if ((dtype != DPPO_F32 && dtype != DPPO_BF16) || V < 1 || ld < V) return nullptr;
   const bool aligned = (ld * esize_of(dtype)) % 16 == 0;
-  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, with_dlogits != 0, g_path_policy);
+  const dppo::RowLaunch L =
+      dppo::select_row_kernel(dtype, V, aligned, with_dlogits != 0, g_path_policy, true);
   thread_local char buf[96];
   const char* ty = dtype == DPPO_BF16 ? "bf16" : "f32";
   const char* bw = with_dlogits ? "true" : "false";
   if (L.prefix)
     snprintf(buf, sizeof(buf), "dppo::rows_%s_prefix<%d, %d>", ty, L.threads, L.chunks);
+  else if (L.phase && !with_dlogits)
+    snprintf(buf, sizeof(buf), "dppo::rows_bf16_fwd_phase<%d, %d>", L.threads, L.chunks);
+  else if (L.phase && L.two_buffers)
+    snprintf(buf, sizeof(buf), "dppo::rows_bf16_phase_db<%d, %d>", L.threads, L.chunks);
+  else if (L.phase)
+    snprintf(buf, sizeof(buf), "dppo::rows_bf16_phase<%d, %d, true>", L.threads, L.chunks);
   else if (L.resident && dtype == DPPO_BF16 && !with_dlogits)
     snprintf(buf, sizeof(buf), "dppo::rows_bf16_fwd<%d, %d>", L.threads, L.chunks);
   else if (L.two_buffers)
@@ -355,7 +362,8 @@ dppo_status logprob_fwd(const void* logits, int32_t dtype, int64_t T, int64_t V,
   if (T == 0) return DPPO_OK;
   const int es = esize_of(dtype);
   const bool aligned = aligned16(logits) && ((ld * es) % 16 == 0);
-  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
+  const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy,
+                                                    ((uintptr_t)logits & 1) == 0);
   dppo::RowArgsV a{};
   a.logits = logits;
   a.ld = ld;
@@ -387,8 +395,12 @@ dppo_status logprob_fwd_versioned(const void* const* logits, int32_t K, int32_t 
     return fail(DPPO_ERR_INVALID_ARG, "version_ids, token_ids and logp_out are required");
   const int es = esize_of(dtype);
   bool aligned = (ld * es) % 16 == 0;
-  for (int v = 0; v < K; ++v) aligned = aligned && aligned16(logits[v]);
-  dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy);
+  bool even = true;
+  for (int v = 0; v < K; ++v) {
+    aligned = aligned && aligned16(logits[v]);
+    even = even && ((uintptr_t)logits[v] & 1) == 0;
+  }
+  dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, false, g_path_policy, even);
   // Rows gathered from several versions' logits want every slot of the device: at
   // 1024 x 19 (bf16, V = 151936, 4 versions) 32 of 32 slots took 0.753-0.757 ms against
   // 0.762-0.768 ms with the 30 that suit one matrix (same-box sweep).
@@ -435,7 +447,13 @@ dppo_status decoupled_ppo_loss_fwd_bwd(
   if (T > 0) {
     const bool aligned = aligned16(logits) && ((ld * es) % 16 == 0) &&
                          (!dlogits || (aligned16(dlogits) && (ld_dlogits * es) % 16 == 0));
-    const dppo::RowLaunch L = dppo::select_row_kernel(dtype, V, aligned, dlogits != nullptr, g_path_policy);
+    // rows with a phase: dlogits row t must start at logits row t's offset within 16 bytes
+    const bool phase_ok =
+        ((uintptr_t)logits & 1) == 0 &&
+        (!dlogits || ((((uintptr_t)dlogits - (uintptr_t)logits) & 15) == 0 &&
+                      (ld_dlogits - ld) % 8 == 0));
+    const dppo::RowLaunch L =
+        dppo::select_row_kernel(dtype, V, aligned, dlogits != nullptr, g_path_policy, phase_ok);
     dppo::RowArgsV a{};
     a.logits = logits;
     a.ld = ld;

@@ -68,13 +68,18 @@ struct RowLaunch {
   bool persistent = false;  // grid = resident workgroups on the device, rows looped over
   bool two_buffers = false; // resident backward kernel with two row buffers
   bool prefix = false;       // backward kernel with a resident prefix and a streamed tail
+  bool phase = false;        // bf16 resident kernel for rows with a phase (rows_bf16_*phase*)
   int fill = 27;             // persistent grids: workgroups launched per 32 resident slots
   int stagger = 2;           // RowArgs::stagger for the kernels that stagger their starts
 };
 
 constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the prefix kernels
 
-RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force);
+// aligned: the rows (and dlogits rows) start on 16-byte boundaries. phase_ok: bf16 rows that
+// start anywhere (2-byte aligned), with dlogits (if any) at the logits' phase on every row;
+// rows that are not aligned or not a whole number of chunks then use the phase kernels.
+RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force,
+                            bool phase_ok = false);
 void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream_t st);
 void launch_loss_sum(const float* loss_tok, const uint8_t* mask, const float* tscale,
                      const int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,

@@ -145,7 +145,15 @@ __device__ __forceinline__ void finish_row(const RowArgs& a, int64_t row, float 
 // workgroup's next row streams in while its current row is reduced and stored (5-10 %
 // faster for the shapes 512 x 4 .. 1024 x 8 on MI355X).
 // ---------------------------------------------------------------------------------------
-template <int NT, int NC, bool BWD, bool DB>
+// With PH (rows that do not start on a 16-byte boundary, or whose length is not a whole number
+// of chunks) a row is read as the aligned chunks that cover it, from the 16-byte boundary at
+// or below its start: the first ph = (start / 2) % 8 entries of the first chunk belong to the
+// row before, and the last chunk may run past the row's end (at most 7 entries, inside the
+// 16-byte boundary after it). Those entries are read but count as -inf in the sums, and are
+// never written: the first and last chunks of the gradient are stored entry by entry, so the
+// neighbouring rows (other workgroups' dlogits, or their logits in place) are left alone.
+// dlogits must then have the logits' phase on every row (the launcher checks it).
+template <int NT, int NC, bool BWD, bool DB, bool PH>
 __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   __shared__ float red[2][2 * (NT / 64)];   // alternated merge by merge: one barrier per merge
   __shared__ Bcast bc;
@@ -165,6 +173,17 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   // Every load and store of the row goes through a buffer resource; a resource with
   // num_records = 0 turns an access into a no-op (loads read zeros, stores are dropped),
   // which keeps the chunk loops free of branches.
+  // The resource over row rr's chunks (size 0 when rd is false); with PH it starts at the
+  // 16-byte boundary at or below the row and covers the chunks the row touches.
+  auto load_rsrc = [&](int64_t rr, bool rd) -> __amdgpu_buffer_rsrc_t {
+    const uint16_t* p = row_ptr<uint16_t>(a, rd ? rr : 0);
+    if constexpr (PH) {
+      const int ph = (int)(((uintptr_t)p >> 1) & 7);
+      return row_rsrc(p - ph, rd ? ((ph + a.V + 7) >> 3) * 16 : 0);
+    } else {
+      return row_rsrc(p, rd ? a.V * 2 : 0);
+    }
+  };
   uint32_t r1[NC][4];
   uint32_t r2[DB ? NC : 1][4];             // the second row buffer (DB)
   StatCount sc;                            // thread 0's counters over this workgroup's rows
@@ -180,8 +199,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   }
   bool rd_cur = row < a.T && reads(row);
   {
-    const __amdgpu_buffer_rsrc_t rz =
-        row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rz = load_rsrc(row, rd_cur);
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16<kAuxLast>(r1[c], rz, threadIdx.x * 16, c * NT * 16);
   }
@@ -207,11 +225,15 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     // range check) and are dropped from the sums and from the stores.
     const int cb = nfull / NT;
     const bool lane_in = tid < nfull - cb * NT;
+    // PH: the row's phase; entry k of this thread's chunk in slot c lies inside the row iff
+    // ph_lo(c) <= k < ph_hi(c).
+    const int ph = PH ? (int)(((uintptr_t)row_ptr<uint16_t>(a, row) >> 1) & 7) : 0;
+    auto ph_lo = [&](int c) { return ph - 8 * (c * NT + tid); };
+    auto ph_hi = [&](int c) { return ph + V - 8 * (c * NT + tid); };
 
     const int64_t next = row + gridDim.x;
     const bool rd_next = next < a.T && reads(next);
-    const __amdgpu_buffer_rsrc_t rn = row_rsrc(
-        row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rn = load_rsrc(rd_next ? next : row, rd_next);
     if constexpr (DB) {
 #pragma unroll
       for (int c = 0; c < NC; ++c) load16<kAuxLast>(nx[c], rn, voff, c * NT * 16);
@@ -226,9 +248,9 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
       // are written, in place, only by this workgroup and only after this read.
       float zy = 0.0f;
       if (good) {
-        const uint64_t off = (uint64_t)(row * a.ld + y) * 2u;
-        const uint32_t wv = uload((const uint32_t*)((const char*)logits_of(a, row) + (off & ~(uint64_t)3)));
-        zy = (off & 2u) ? bf16_hi(wv) : bf16_lo(wv);
+        const uintptr_t at = (uintptr_t)logits_of(a, row) + (uintptr_t)(row * a.ld + y) * 2u;
+        const uint32_t wv = uload((const uint32_t*)(at & ~(uintptr_t)3));
+        zy = (at & 2u) ? bf16_hi(wv) : bf16_lo(wv);
       }
       // Pass A.
       float N = -INFINITY, S = 0.0f;
@@ -240,6 +262,11 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
           x[2 * k] = bf16_lo(r[c][k]);
           x[2 * k + 1] = bf16_hi(r[c][k]);
         }
+        if constexpr (PH) {                 // entries of the neighbouring rows
+          const int lo = ph_lo(c), hi = ph_hi(c);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) x[k] = (k >= lo && k < hi) ? x[k] : -INFINITY;
+        }
         const float cm = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
         float nc = __builtin_ceilf(cm * kLog2e);
         const float sh = (nc == -INFINITY) ? 0.0f : nc;
@@ -248,7 +275,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
         for (int j = 0; j < 8; ++j) e[j] = exp2_hw(__builtin_fmaf(x[j], kLog2e, -sh));
         float sc = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
         // a chunk outside the row contributes nothing
-        const bool dead = (c > cb) || (c == cb && !lane_in);
+        const bool dead = PH ? ph_hi(c) <= 0 : ((c > cb) || (c == cb && !lane_in));
         nc = dead ? -INFINITY : nc;
         sc = dead ? 0.0f : sc;
         if (BWD) {
@@ -299,8 +326,29 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     // next row's chunks. For a row that was not read the dlogits stores are dropped and
     // zeros are written below.
     uint16_t* drow = want_d ? (uint16_t*)a.dlogits + row * a.ldd : nullptr;
-    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, (want_d && rd_cur) ? V * 2 : 0);
+    // PH: a resource from the 16-byte boundary at or below the row, over the chunks it
+    // touches (dlogits has the logits' phase)
+    uint16_t* dbase = PH ? drow - ph : drow;
+    const int dbytes = PH ? ((ph + V + 7) >> 3) * 16 : V * 2;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(dbase, (want_d && rd_cur) ? dbytes : 0);
     const float wf = rd_cur ? w : 0.0f;
+    // PH: chunk c is stored whole when it lies inside the row, else entry by entry
+    auto store_chunk = [&](const u32x4& v, const __amdgpu_buffer_rsrc_t& res, int c) {
+      if constexpr (PH) {
+        const int lo = ph_lo(c), hi = ph_hi(c);
+        if (lo <= 0 && hi >= 8) {
+          buf_store16_nt(v, res, voff, c * NT * 16);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            if (k >= lo && k < hi)
+              __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(v[k >> 1] >> (16 * (k & 1))), res,
+                                                    voff + 2 * k, c * NT * 16, kAuxNT);
+        }
+      } else {
+        buf_store16_nt(v, res, voff, c * NT * 16);
+      }
+    };
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       if (BWD) {
@@ -320,7 +368,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
         v.y = pack_bf16(o[2], o[3]);
         v.z = pack_bf16(o[4], o[5]);
         v.w = pack_bf16(o[6], o[7]);
-        buf_store16_nt(v, rd, voff, c * NT * 16);
+        store_chunk(v, rd, c);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -332,16 +380,16 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
       for (int c = 0; c < NC; ++c) load16<kAuxLast>(nx[c], rn, voff, c * NT * 16);
     }
     if (want_d && !rd_cur) {                // zeros for a row that was not read
-      const __amdgpu_buffer_rsrc_t rz = row_rsrc(drow, V * 2);
+      const __amdgpu_buffer_rsrc_t rz = row_rsrc(dbase, dbytes);
       const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int c = 0; c < NC; ++c) buf_store16_nt(zero, rz, voff, c * NT * 16);
+      for (int c = 0; c < NC; ++c) store_chunk(zero, rz, c);
     }
     // dlogits at v = y is w (p_y - 1) = w expm1(lp), computed once by thread 0. The thread
     // whose chunk holds y writes it over its own vector store above: two stores of one
     // thread to one address, through the same buffer path, land in program order.
-    if (want_d && rd_cur && good && tid == (int)((y >> 3) % NT))
-      __builtin_amdgcn_raw_buffer_store_b16(to_bf16(dy), rd, (int)(y * 2), 0, kAuxNT);
+    if (want_d && rd_cur && good && tid == (int)(((y + ph) >> 3) % NT))
+      __builtin_amdgcn_raw_buffer_store_b16(to_bf16(dy), rd, (int)((y + ph) * 2), 0, kAuxNT);
     rd_cur = rd_next;
   };
   if constexpr (DB) {
@@ -364,12 +412,21 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
 
 template <int NT, int NC, bool BWD>
 __global__ __launch_bounds__(NT) void rows_bf16_resident(RowArgsOf<BWD> a) {
-  resident_rows<NT, NC, BWD, false>(a);
+  resident_rows<NT, NC, BWD, false, false>(a);
+}
+// Rows with a phase (see resident_rows).
+template <int NT, int NC, bool BWD>
+__global__ __launch_bounds__(NT) void rows_bf16_phase(RowArgsOf<BWD> a) {
+  resident_rows<NT, NC, BWD, false, true>(a);
 }
 // The two-buffer form, with dlogits (the backward kernel).
 template <int NT, int NC>
 __global__ __launch_bounds__(NT) void rows_bf16_resident_db(RowArgs a) {
-  resident_rows<NT, NC, true, true>(a);
+  resident_rows<NT, NC, true, true, false>(a);
+}
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_bf16_phase_db(RowArgs a) {
+  resident_rows<NT, NC, true, true, true>(a);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -381,11 +438,21 @@ __global__ __launch_bounds__(NT) void rows_bf16_resident_db(RowArgs a) {
 // top. Rows that are not read (masked or bad-id loss rows) still run the chunk loop on
 // zeros, so that every row issues its successor's loads from the same place.
 // ---------------------------------------------------------------------------------------
-template <int NT, int NC>
-__global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
+// PH: rows with a phase, read as in resident_rows.
+template <int NT, int NC, bool PH>
+__device__ __forceinline__ void fwd_rows(const RowArgsV& a) {
   __shared__ float red[2][2 * (NT / 64)];
   __shared__ Bcast bc;
   const bool loss_mode = a.mode != kModeLogprob;
+  auto load_rsrc = [&](int64_t rr, bool rd) -> __amdgpu_buffer_rsrc_t {
+    const uint16_t* p = row_ptr<uint16_t>(a, rd ? rr : 0);
+    if constexpr (PH) {
+      const int ph = (int)(((uintptr_t)p >> 1) & 7);
+      return row_rsrc(p - ph, rd ? ((ph + a.V + 7) >> 3) * 16 : 0);
+    } else {
+      return row_rsrc(p, rd ? a.V * 2 : 0);
+    }
+  };
   auto reads = [&](int64_t rr) -> bool {
     if (!loss_mode) return true;
     if (a.mask != nullptr && uload_u8(a.mask + rr) == 0) return false;
@@ -401,8 +468,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
   }
   bool rd_cur = row < a.T && reads(row);
   {
-    const __amdgpu_buffer_rsrc_t rz =
-        row_rsrc(row_ptr<uint16_t>(a, rd_cur ? row : 0), rd_cur ? a.V * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rz = load_rsrc(row, rd_cur);
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16<kAuxLast>(r[c], rz, threadIdx.x * 16, c * NT * 16);
   }
@@ -415,18 +481,18 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
     const int nfull = V >> 3;
     const int cb = nfull / NT;
     const bool lane_in = tid < nfull - cb * NT;
+    const int ph = PH ? (int)(((uintptr_t)row_ptr<uint16_t>(a, row) >> 1) & 7) : 0;
     const int64_t next = row + gridDim.x;
     const bool rd_next = next < a.T && reads(next);
-    const __amdgpu_buffer_rsrc_t rn =
-        row_rsrc(row_ptr<uint16_t>(a, rd_next ? next : row), rd_next ? V * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rn = load_rsrc(rd_next ? next : row, rd_next);
     const int64_t y = uload(a.ids + row);
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
     const TokenIn tin = token_inputs(a, row);
     float zy = 0.0f;
     if (rd_cur && good) {
-      const uint64_t off = (uint64_t)(row * a.ld + y) * 2u;
-      const uint32_t wv = uload((const uint32_t*)((const char*)logits_of(a, row) + (off & ~(uint64_t)3)));
-      zy = (off & 2u) ? bf16_hi(wv) : bf16_lo(wv);
+      const uintptr_t at = (uintptr_t)logits_of(a, row) + (uintptr_t)(row * a.ld + y) * 2u;
+      const uint32_t wv = uload((const uint32_t*)(at & ~(uintptr_t)3));
+      zy = (at & 2u) ? bf16_hi(wv) : bf16_lo(wv);
     }
     float N = -INFINITY, S = 0.0f;
 #pragma unroll
@@ -438,6 +504,11 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
         x[2 * k + 1] = bf16_hi(r[c][k]);
       }
       load16<kAuxLast>(r[c], rn, voff, c * NT * 16);
+      const int lo = ph - 8 * (c * NT + tid), hi = ph + V - 8 * (c * NT + tid);
+      if constexpr (PH) {                   // entries of the neighbouring rows
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[k] = (k >= lo && k < hi) ? x[k] : -INFINITY;
+      }
       const float cm = max3(max3(x[0], x[1], x[2]), max3(x[3], x[4], x[5]), max3(x[6], x[7], x[7]));
       float nc = __builtin_ceilf(cm * kLog2e);
       const float sh = (nc == -INFINITY) ? 0.0f : nc;
@@ -447,7 +518,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) e[j] = exp2_hw(__builtin_fmaf(x[j], kLog2e, -sh));
       const float sc = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-      const bool dead = (c > cb) || (c == cb && !lane_in);
+      const bool dead = PH ? hi <= 0 : ((c > cb) || (c == cb && !lane_in));
       merge_ns_int(N, S, dead ? -INFINITY : nc, dead ? 0.0f : sc);
       // Pin the chunk's work here: otherwise the exponentials are sunk past the later
       // chunks and every chunk's unpacked values stay live at once.
@@ -469,6 +540,15 @@ __global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
     rd_cur = rd_next;
   }
   if (threadIdx.x == 0) flush_stats(a, sc);
+}
+
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_bf16_fwd(RowArgsV a) {
+  fwd_rows<NT, NC, false>(a);
+}
+template <int NT, int NC>
+__global__ __launch_bounds__(NT) void rows_bf16_fwd_phase(RowArgsV a) {
+  fwd_rows<NT, NC, true>(a);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -1196,6 +1276,45 @@ const void* pick_bf16_fwd(int i) {
     default: return (const void*)rows_bf16_fwd<1024, 19>;
   }
 }
+const void* pick_bf16_fwd_phase(int i) {
+  switch (i) {
+    case 0: return (const void*)rows_bf16_fwd_phase<256, 1>;
+    case 1: return (const void*)rows_bf16_fwd_phase<256, 2>;
+    case 2: return (const void*)rows_bf16_fwd_phase<256, 4>;
+    case 3: return (const void*)rows_bf16_fwd_phase<512, 4>;
+    case 4: return (const void*)rows_bf16_fwd_phase<512, 6>;
+    case 5: return (const void*)rows_bf16_fwd_phase<512, 8>;
+    case 6: return (const void*)rows_bf16_fwd_phase<1024, 6>;
+    case 7: return (const void*)rows_bf16_fwd_phase<1024, 8>;
+    case 8: return (const void*)rows_bf16_fwd_phase<1024, 12>;
+    default: return (const void*)rows_bf16_fwd_phase<1024, 19>;
+  }
+}
+const void* pick_bf16_phase_db(int i) {
+  switch (i) {
+    case 3: return (const void*)rows_bf16_phase_db<512, 4>;
+    case 4: return (const void*)rows_bf16_phase_db<512, 6>;
+    case 5: return (const void*)rows_bf16_phase_db<512, 8>;
+    case 6: return (const void*)rows_bf16_phase_db<1024, 6>;
+    case 7: return (const void*)rows_bf16_phase_db<1024, 8>;
+    default: return nullptr;
+  }
+}
+template <bool BWD>
+const void* pick_bf16_phase(int i) {
+  switch (i) {
+    case 0: return (const void*)rows_bf16_phase<256, 1, BWD>;
+    case 1: return (const void*)rows_bf16_phase<256, 2, BWD>;
+    case 2: return (const void*)rows_bf16_phase<256, 4, BWD>;
+    case 3: return (const void*)rows_bf16_phase<512, 4, BWD>;
+    case 4: return (const void*)rows_bf16_phase<512, 6, BWD>;
+    case 5: return (const void*)rows_bf16_phase<512, 8, BWD>;
+    case 6: return (const void*)rows_bf16_phase<1024, 6, BWD>;
+    case 7: return (const void*)rows_bf16_phase<1024, 8, BWD>;
+    case 8: return (const void*)rows_bf16_phase<1024, 12, BWD>;
+    default: return (const void*)rows_bf16_phase<1024, 19, BWD>;
+  }
+}
 // Two-buffer backward kernels, for the shapes kResidentDB selects.
 const void* pick_bf16_db(int i) {
   switch (i) {
@@ -1239,14 +1358,19 @@ const void* pick_f32(int i) {
 }
 }  // namespace
 
-RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force) {
+RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force,
+                            bool phase_ok) {
   RowLaunch L;
   L.bwd = bwd;
   const int esize = dtype == DPPO_BF16 ? 2 : 4;
-  const int64_t chunks = (V * esize + 15) / 16;
+  int64_t chunks = (V * esize + 15) / 16;
   int pick = -1;
   const bool whole_chunks = (V * esize) % 16 == 0;
-  if (aligned && whole_chunks && force != kForceStream) {
+  // a row with a phase touches at most ceil((V + 7) / 8) chunks (ceil(V / 8) when every row
+  // starts on a 16-byte boundary)
+  const bool ph = !(aligned && whole_chunks) && dtype == DPPO_BF16 && phase_ok;
+  if (ph && !aligned) chunks = (V + 14) / 8;
+  if (((aligned && whole_chunks) || ph) && force != kForceStream) {
     for (int i = 0; i < kNumResident; ++i) {
       if ((int64_t)kResident[i].nt * kResident[i].nc >= chunks) {
         pick = i;
@@ -1257,10 +1381,15 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   if (pick >= 0) {
     L.threads = kResident[pick].nt;
     L.chunks = kResident[pick].nc;
-    L.fn = dtype == DPPO_BF16
-               ? (bwd ? (kResidentDB[pick] ? pick_bf16_db(pick) : pick_bf16<true>(pick))
-                      : pick_bf16_fwd(pick))
-               : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
+    L.phase = ph;
+    if (dtype == DPPO_BF16 && ph)
+      L.fn = bwd ? (kResidentDB[pick] ? pick_bf16_phase_db(pick) : pick_bf16_phase<true>(pick))
+                 : pick_bf16_fwd_phase(pick);
+    else
+      L.fn = dtype == DPPO_BF16
+                 ? (bwd ? (kResidentDB[pick] ? pick_bf16_db(pick) : pick_bf16<true>(pick))
+                        : pick_bf16_fwd(pick))
+                 : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
     L.two_buffers = dtype == DPPO_BF16 && bwd && kResidentDB[pick];
     L.resident = true;
     L.persistent = dtype == DPPO_BF16 || kF32Persistent[pick];

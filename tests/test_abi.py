@@ -304,8 +304,10 @@ def test_host_ewma_proxy_decisions_follow_the_library(monkeypatch):
 
 def test_row_kernel_name_follows_the_selection_rule():
     """Host-only query: the resident kernel while a row fits NT x NC 16-byte chunks (at most
-    1024 x 19 x 8 = 155648 bf16 elements) with whole chunks; beyond, the resident-prefix
-    kernel for aligned rows with dlogits, the streaming kernel otherwise."""
+    1024 x 19 x 8 = 155648 bf16 elements) with whole chunks; bf16 rows that are unaligned or
+    ragged use the phase kernels while the chunks they touch (ceil((V + 7) / 8), or ceil(V / 8)
+    on an aligned stride) fit; beyond, the resident-prefix kernel for aligned rows with
+    dlogits, the streaming kernel otherwise."""
     import torch
     from paper_2605_12070_amd import row_kernel_name
     bf, f32 = torch.bfloat16, torch.float32
@@ -320,8 +322,14 @@ def test_row_kernel_name_follows_the_selection_rule():
     assert row_kernel_name(bf, 151936, with_dlogits=False) == "dppo::rows_bf16_fwd<1024, 19>"
     assert row_kernel_name(f32, 32000, with_dlogits=False) == "dppo::rows_f32_resident<1024, 8, false>"
     assert row_kernel_name(bf, 2048) == "dppo::rows_bf16_resident<256, 1, true>"
-    assert row_kernel_name(bf, 77825).startswith("dppo::rows_stream")      # ragged chunk
-    assert row_kernel_name(bf, 64, ld=68).endswith("true, false>")          # unaligned stride
+    assert row_kernel_name(bf, 77825) == "dppo::rows_bf16_phase<1024, 12, true>"  # ragged
+    assert row_kernel_name(bf, 64, ld=68) == "dppo::rows_bf16_phase<256, 1, true>"  # unaligned
+    assert row_kernel_name(bf, 50257) == "dppo::rows_bf16_phase_db<1024, 8>"
+    assert row_kernel_name(bf, 50257, with_dlogits=False) == "dppo::rows_bf16_fwd_phase<1024, 8>"
+    assert row_kernel_name(bf, 151665, ld=151936) == "dppo::rows_bf16_phase<1024, 19, true>"
+    assert row_kernel_name(bf, 155647, ld=155648) == "dppo::rows_bf16_phase<1024, 19, true>"
+    assert row_kernel_name(bf, 155641) == "dppo::rows_bf16_phase<1024, 19, true>"
+    assert row_kernel_name(bf, 155642).startswith("dppo::rows_stream")     # up to 7 more chunks
     assert row_kernel_name(f32, 32000) == "dppo::rows_f32_resident<1024, 8, true>"
     # fp32 rows past the resident kernels: a resident prefix and a streamed tail when the
     # row holds at least the prefix's 1024 x 19 whole chunks; otherwise the streaming kernel

@@ -1,0 +1,125 @@
+"""bf16 rows that do not start on a 16-byte boundary or are not a whole number of 16-byte
+chunks long: the phase kernels read each row as the aligned chunks that cover it and write
+only the row's own entries. Every case compares lp, loss_tok, flags and dlogits with the
+oracle, and checks that every byte of the buffers outside the rows is left as it was
+(the entries between rows, before the first row and after the last)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_12070_amd as P
+
+from helpers import compare_loss, oracle_anchor, oracle_params, run_oracle
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+SENTINEL = 7.0                      # exactly representable in bf16
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _inputs(T, V, ld, off, seed):
+    """Logits rows of length V at element offset `off` of a buffer, row stride ld; ids with
+    the first and last entries of rows, a bad id, masked rows."""
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    n = off + T * ld + 16
+    buf = (torch.randn(n, generator=g, device=DEV) * 3).to(torch.bfloat16)
+    z = buf[off:off + T * ld].view(T, ld)[:, :V]
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[0] = V - 1
+    ids[1] = 0
+    if T > 5:
+        ids[5] = V + 3                   # bad id on a valid row
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    mask[3::7] = 0
+    anchor = oracle_anchor(z, ids.clamp(0, V - 1)).to(DEV)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.1 * torch.randn(T, generator=g, device=DEV,
+                                                 dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    return buf, z, ids, mask, lp_mu, lp_ref, adv
+
+
+def _outside(buf, off, T, ld, V):
+    """Boolean mask of the buffer entries that belong to no row."""
+    m = torch.ones(buf.numel(), dtype=torch.bool, device=buf.device)
+    rows = off + torch.arange(T, device=buf.device)[:, None] * ld + torch.arange(V, device=buf.device)[None, :]
+    m[rows.reshape(-1)] = False
+    return m
+
+
+CASES = [  # T, V, extra columns per row, element offset of row 0
+    (40, 1, 0, 3), (40, 9, 0, 1), (300, 1003, 0, 0), (300, 1003, 5, 7), (200, 5003, 3, 1),
+    (600, 8192, 1, 0), (120, 32001, 0, 5), (64, 50257, 0, 0), (64, 50257, 47, 2),
+    (24, 151665, 271, 0), (24, 151937, 0, 6), (12, 155641, 0, 7),
+]
+
+
+@pytest.mark.parametrize("T,V,extra,off", CASES, ids=[f"T{c[0]}_V{c[1]}_x{c[2]}_o{c[3]}" for c in CASES])
+def test_phase_rows_loss_and_untouched_neighbours(T, V, extra, off):
+    ld = V + extra
+    _say("phase rows", T, V, ld, off)
+    buf, z, ids, mask, lp_mu, lp_ref, adv = _inputs(T, V, ld, off, seed=V + off)
+    name = P.row_kernel_name(torch.bfloat16, V, ld)
+    if (ld % 8 == 0) and (V % 8 == 0):
+        assert "phase" not in name
+    else:
+        assert "phase" in name or "prefix" in name, name
+    # dlogits into a second buffer with the same layout, filled with a sentinel
+    dbuf = torch.full_like(buf, SENTINEL)
+    d = dbuf[off:off + T * ld].view(T, ld)[:, :V]
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, dlogits=d,
+                                       scale_mode="const")
+    torch.cuda.synchronize()
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    compare_loss(res, ref, params, torch.bfloat16)
+    out = _outside(dbuf, off, T, ld, V)
+    assert torch.all(dbuf[out] == SENTINEL), "entries outside the rows were written"
+    # in place: the gradient overwrites the rows, and only the rows
+    zin = buf.clone()
+    zz = zin[off:off + T * ld].view(T, ld)[:, :V]
+    res2 = P.decoupled_ppo_loss_fwd_bwd(zz, ids, lp_mu, lp_ref, adv, mask, dlogits=zz,
+                                        scale_mode="const")
+    torch.cuda.synchronize()
+    assert torch.equal(zz.view(torch.int16), d.view(torch.int16)), "in place differs"
+    assert torch.equal(zin[out].view(torch.int16), buf[out].view(torch.int16))
+    assert torch.equal(res2.logp.view(torch.int32), res.logp.view(torch.int32))
+
+
+@pytest.mark.parametrize("T,V,extra,off", CASES[:8], ids=[f"T{c[0]}_V{c[1]}_x{c[2]}_o{c[3]}" for c in CASES[:8]])
+def test_phase_rows_forward_only(T, V, extra, off):
+    ld = V + extra
+    _say("phase rows forward", T, V, ld, off)
+    buf, z, ids, mask, lp_mu, lp_ref, adv = _inputs(T, V, ld, off, seed=3 * V + off)
+    lp = P.logprob_fwd(z, ids.clamp(0, V - 1))
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, want_dlogits=False,
+                                       scale_mode="const")
+    torch.cuda.synchronize()
+    ref_lp, _ = oracle.logprob_fwd(oracle.bf16_bits_to_f64(
+        z.cpu().view(torch.int16).numpy().view(np.uint16)), ids.clamp(0, V - 1).cpu().numpy())
+    got = lp.cpu().double().numpy()
+    assert np.all(np.abs(got - ref_lp) <= 2e-5 * np.maximum(np.abs(ref_lp), 1.0))
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params, want_dlogits=False)
+    compare_loss(res, ref, params, torch.bfloat16, check_dlogits=False)
+
+
+def test_phase_rows_with_a_mismatched_gradient_layout_take_the_streaming_path():
+    """dlogits at another offset within 16 bytes than the logits: the phase kernels cannot
+    serve it, the streaming kernel does, with the same results."""
+    T, V, ld, off = 50, 1003, 1003, 1
+    buf, z, ids, mask, lp_mu, lp_ref, adv = _inputs(T, V, ld, off, seed=99)
+    dbuf = torch.full((off + 1 + T * ld + 16,), SENTINEL, dtype=torch.bfloat16, device=DEV)
+    d = dbuf[off + 1:off + 1 + T * ld].view(T, ld)[:, :V]
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, dlogits=d,
+                                       scale_mode="const")
+    torch.cuda.synchronize()
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    compare_loss(res, ref, params, torch.bfloat16)
+    out = _outside(dbuf, off + 1, T, ld, V)
+    assert torch.all(dbuf[out] == SENTINEL)
