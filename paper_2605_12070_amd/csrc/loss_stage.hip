@@ -1370,7 +1370,10 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   // starts on a 16-byte boundary)
   const bool ph = !(aligned && whole_chunks) && dtype == DPPO_BF16 && phase_ok;
   if (ph && !aligned) chunks = (V + 14) / 8;
-  if (((aligned && whole_chunks) || ph) && force != kForceStream) {
+  // fp32 rows on an aligned stride may end in a partial chunk: rows_f32_resident loads and
+  // stores its last V % 4 entries one by one
+  const bool f32_ragged = dtype == DPPO_F32 && aligned && !whole_chunks;
+  if (((aligned && whole_chunks) || ph || f32_ragged) && force != kForceStream) {
     for (int i = 0; i < kNumResident; ++i) {
       if ((int64_t)kResident[i].nt * kResident[i].nc >= chunks) {
         pick = i;

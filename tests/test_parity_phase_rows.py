@@ -108,6 +108,51 @@ def test_phase_rows_forward_only(T, V, extra, off):
     compare_loss(res, ref, params, torch.bfloat16, check_dlogits=False)
 
 
+F32_CASES = [(300, 1003, 1), (200, 5003, 1), (120, 32001, 3), (40, 77821, 3)]
+
+
+@pytest.mark.parametrize("T,V,extra", F32_CASES, ids=[f"T{c[0]}_V{c[1]}_x{c[2]}" for c in F32_CASES])
+def test_fp32_ragged_rows_on_an_aligned_stride(T, V, extra):
+    """fp32 rows whose length is not a multiple of 4 on a 16-byte stride: the resident kernel
+    with its last entries loaded and stored one by one; the stride's padding is left alone."""
+    ld = V + extra
+    assert ld % 4 == 0
+    _say("fp32 ragged rows", T, V, ld)
+    assert P.row_kernel_name(torch.float32, V, ld).startswith("dppo::rows_f32_resident")
+    g = torch.Generator(device=DEV).manual_seed(V)
+    buf = torch.randn(T * ld, generator=g, device=DEV) * 3
+    z = buf.view(T, ld)[:, :V]
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[0] = V - 1
+    ids[2] = V - 2
+    ids[5] = -1
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    mask[3::7] = 0
+    anchor = oracle_anchor(z, ids.clamp(0, V - 1)).to(DEV)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.1 * torch.randn(T, generator=g, device=DEV,
+                                                 dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    dbuf = torch.full_like(buf, SENTINEL)
+    d = dbuf.view(T, ld)[:, :V]
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, dlogits=d,
+                                       scale_mode="const")
+    lp = P.logprob_fwd(z, ids.clamp(0, V - 1))
+    torch.cuda.synchronize()
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    compare_loss(res, ref, params, torch.float32)
+    assert torch.all(dbuf.view(T, ld)[:, V:] == SENTINEL)
+    ref_lp, _ = oracle.logprob_fwd(z.cpu().double().numpy(), ids.clamp(0, V - 1).cpu().numpy())
+    assert np.all(np.abs(lp.cpu().double().numpy() - ref_lp) <= 1e-5 * np.maximum(np.abs(ref_lp), 1.0))
+    # in place
+    zz = buf.clone().view(T, ld)
+    P.decoupled_ppo_loss_fwd_bwd(zz[:, :V], ids, lp_mu, lp_ref, adv, mask, dlogits=zz[:, :V],
+                                 scale_mode="const")
+    torch.cuda.synchronize()
+    assert torch.equal(zz[:, :V], d) and torch.equal(zz[:, V:], buf.view(T, ld)[:, V:])
+
+
 def test_phase_rows_with_a_mismatched_gradient_layout_take_the_streaming_path():
     """dlogits at another offset within 16 bytes than the logits: the phase kernels cannot
     serve it, the streaming kernel does, with the same results."""
