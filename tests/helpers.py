@@ -78,10 +78,21 @@ def assert_close_rel(gpu, ref, rtol, what, floor=1.0, mask=None):
     return worst
 
 
-def check_dlogits_rows(gpu_rows, ref_rows, w, out_dtype, what="dlogits"):
-    """gpu_rows: float64 values of the kernel's dlogits rows; ref_rows: oracle float64."""
+def check_dlogits_rows(gpu_rows, ref_rows, w, out_dtype, what="dlogits", lp=None):
+    """gpu_rows: float64 values of the kernel's dlogits rows; ref_rows: oracle float64.
+    With lp (the oracle's log-probs of the rows), the sampled entry w (p_y - 1), the one entry
+    whose sign is opposite to w's, may also be off by |w| p_y TIGHT max(|lp|, 1): it carries
+    the log-prob's own absolute error (the TIGHT bound of the lp check) through p_y, which a
+    bound relative to |p_y - 1| does not cover once p_y is close to 1 (a vocabulary of a
+    few entries, or a confident token)."""
     drel = 2.0 ** -8 + 2.0 ** -11 if out_dtype == torch.bfloat16 else 2e-5
     bound = drel * np.abs(ref_rows) + 2.0 ** -22 * np.abs(w)[:, None] + 1e-30
+    if lp is not None:
+        wy = np.asarray(w)[:, None]
+        ysel = (ref_rows * wy) < 0
+        p_y = np.exp(np.minimum(np.nan_to_num(np.asarray(lp, dtype=np.float64)), 0.0))[:, None]
+        ytol = np.abs(wy) * p_y * TIGHT * np.maximum(np.abs(np.nan_to_num(np.asarray(lp)))[:, None], 1.0)
+        bound = bound + np.where(ysel, ytol, 0.0)
     nan_ref = np.isnan(ref_rows)
     assert np.array_equal(np.isnan(gpu_rows), nan_ref), f"{what}: NaN pattern differs"
     err = np.where(nan_ref, 0.0, np.abs(gpu_rows - ref_rows))
@@ -147,5 +158,5 @@ def compare_loss(res, ref, params, logits_dtype, dl_dtype=None, check_dlogits=Tr
         r2 = ref["dlogits"].copy()
         g2[tie_rows] = 0.0
         r2[tie_rows] = 0.0
-        check_dlogits_rows(g2, r2, w, dl_dtype or logits_dtype)
+        check_dlogits_rows(g2, r2, w, dl_dtype or logits_dtype, lp=ref["lp"])
     return int(ties.sum())

@@ -168,3 +168,68 @@ def test_phase_rows_with_a_mismatched_gradient_layout_take_the_streaming_path():
     compare_loss(res, ref, params, torch.bfloat16)
     out = _outside(dbuf, off + 1, T, ld, V)
     assert torch.all(dbuf[out] == SENTINEL)
+
+
+def _random_cases(n=36, seed=2605):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dtype = "bf16" if rng.random() < 0.7 else "f32"
+        V = int(rng.choice([int(rng.integers(1, 64)), int(rng.integers(64, 4096)),
+                            int(rng.integers(4096, 40000)), int(rng.integers(40000, 160000))]))
+        extra = int(rng.choice([0, 0, int(rng.integers(1, 9)), 8 - V % 8]))
+        off = int(rng.choice([0, 0, int(rng.integers(1, 8))]))
+        T = int(max(2, min(400, 3_000_000 // max(V, 1))))
+        out.append((i, dtype, T, V, extra, off, bool(rng.random() < 0.3), bool(rng.random() < 0.25)))
+    return out
+
+
+@pytest.mark.parametrize("i,dtype,T,V,extra,off,in_place,fwd_only", _random_cases(),
+                         ids=[f"{c[0]}_{c[1]}_T{c[2]}_V{c[3]}_x{c[4]}_o{c[5]}" for c in _random_cases()])
+def test_random_layouts_against_the_oracle(i, dtype, T, V, extra, off, in_place, fwd_only):
+    """Seeded random layouts (dtype, V, stride, offset of the first row, T), with masked rows,
+    bad ids, in place or into a second buffer, with or without dlogits: every output against
+    the oracle, and no entry outside the rows written."""
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    ld = V + extra
+    _say("random layout", i, dtype, T, V, ld, off, in_place, fwd_only)
+    g = torch.Generator(device=DEV).manual_seed(1000 + i)
+    n = off + T * ld + 16
+    buf = (torch.randn(n, generator=g, device=DEV) * 3).to(tdt)
+    ref_buf = buf.clone()
+    z = buf[off:off + T * ld].view(T, ld)[:, :V]
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    ids[torch.rand(T, generator=g, device=DEV) < 0.05] = V
+    mask = (torch.rand(T, generator=g, device=DEV) >= 0.15).to(torch.uint8)
+    anchor = oracle_anchor(z, ids.clamp(0, V - 1)).to(DEV)
+    lp_ref = (anchor + 0.2 * torch.randn(T, generator=g, device=DEV, dtype=torch.float64)).float()
+    lp_mu = (lp_ref.double() + 0.1 * torch.randn(T, generator=g, device=DEV,
+                                                 dtype=torch.float64)).float()
+    adv = torch.randn(T, generator=g, device=DEV)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params, want_dlogits=not fwd_only)
+    out = _outside(buf, off, T, ld, V)
+    if fwd_only:
+        res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, want_dlogits=False,
+                                           scale_mode="const")
+        torch.cuda.synchronize()
+        compare_loss(res, ref, params, tdt, check_dlogits=False)
+        assert torch.equal(buf.view(torch.int16) if dtype == "bf16" else buf, ref_buf.view(torch.int16) if dtype == "bf16" else ref_buf)
+        return
+    if in_place:
+        res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, dlogits=z,
+                                           scale_mode="const")
+        torch.cuda.synchronize()
+        compare_loss(res, ref, params, tdt)
+        a, b = buf[out], ref_buf[out]
+    else:
+        dbuf = torch.full_like(buf, SENTINEL)
+        d = dbuf[off:off + T * ld].view(T, ld)[:, :V]
+        res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, dlogits=d,
+                                           scale_mode="const")
+        torch.cuda.synchronize()
+        compare_loss(res, ref, params, tdt)
+        a, b = dbuf[out], torch.full_like(dbuf[out], SENTINEL)
+    if dtype == "bf16":
+        a, b = a.view(torch.int16), b.view(torch.int16)
+    assert torch.equal(a, b), "entries outside the rows were written"
