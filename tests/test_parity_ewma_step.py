@@ -35,11 +35,13 @@ def _rho_of(st):
     return 1.0 if st[0] == 0 else st[3] / st[0]
 
 
+# a buffer of a few workgroups and one of several hundred
+@pytest.mark.parametrize("n", [4099, 140003])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("normalized", [True, False])
 @pytest.mark.parametrize("patience", [1, 2])
-def test_device_step_matches_oracle_and_host_path(dtype, normalized, patience):
-    n, beta, tau = 4099, 0.75, 0.9
+def test_device_step_matches_oracle_and_host_path(dtype, normalized, patience, n):
+    beta, tau = 0.75, 0.9
     _say("ewma step", dtype, normalized, patience, n)
     g = torch.Generator(device=DEV).manual_seed(11 + patience)
     x0 = torch.randn(n, generator=g, device=DEV).to(dtype)
@@ -85,8 +87,8 @@ def test_device_step_matches_oracle_and_host_path(dtype, normalized, patience):
     assert resets == sum(fired_ref) and resets >= 1
 
 
-def test_device_step_bad_normaliser_leaves_everything_unchanged():
-    n = 1000
+@pytest.mark.parametrize("n", [1000, 140003])
+def test_device_step_bad_normaliser_leaves_everything_unchanged(n):
     _say("ewma step bad w", n)
     g = torch.Generator(device=DEV).manual_seed(5)
     x0 = torch.randn(n, generator=g, device=DEV)
