@@ -14,8 +14,8 @@ import oracle
 import paper_2605_12070_amd as P
 from paper_2605_12070_amd import workloads as W
 
-from helpers import (bits_of, compare_loss, oracle_anchor, oracle_params, run_oracle,
-                     tie_mask)
+from helpers import (TIGHT, assert_close_rel, bits_of, compare_loss, oracle_anchor,
+                     oracle_params, run_oracle, tie_mask)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -403,6 +403,71 @@ def test_masked_rows_bad_ids_and_nonfinite_rows():
             st = res.stats.cpu().numpy()
             assert st[P.STAT_N_VALID] == 8 and st[P.STAT_N_BAD] == 1
             assert math.isnan(res.loss.item()) and math.isnan(ref["loss"])
+
+
+# (dtype, V, T): the row kernel families, with T above the persistent grid where the row is
+# short enough for the oracle to take it
+NONFINITE_CASES = [
+    (torch.bfloat16, 32000, 700),     # two-buffer 512 x 8
+    (torch.bfloat16, 151936, 260),    # the flagship 1024 x 19, a second row per workgroup
+    (torch.bfloat16, 50257, 300),     # rows with a phase (odd V)
+    (torch.bfloat16, 262144, 40),     # resident prefix, streamed tail
+    (torch.float32, 76000, 260),      # fp32 1024 x 19
+    (torch.float32, 151936, 40),      # fp32 resident prefix
+    (torch.float32, 32000, 40),       # fp32 one workgroup per row
+]
+
+
+@pytest.mark.parametrize("dtype,V,T", NONFINITE_CASES,
+                         ids=[f"{str(c[0])[6:]}-{c[1]}-{c[2]}" for c in NONFINITE_CASES])
+def test_nonfinite_rows_every_kernel_family(dtype, V, T):
+    """NaN, +inf, all -inf and partly -inf rows, masked rows full of NaN and bad ids, at the
+    start of the batch and again at its end (rows a persistent workgroup reaches after
+    others), with and without dlogits: IEEE propagation as in the oracle."""
+    _say("nonfinite rows", dtype, V, T)
+    g = torch.Generator(device=DEV).manual_seed(V % 1000 + T)
+    z = (torch.randn(T, V, generator=g, device=DEV) * 2).to(dtype)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    mask = torch.ones(T, dtype=torch.uint8, device=DEV)
+    for b in (0, T - 9):
+        z[b + 1, V // 3] = float("nan")    # NaN entry
+        z[b + 2, V - 1] = float("inf")     # +inf entry at the row's end
+        z[b + 3, :] = float("-inf")        # all -inf
+        z[b + 4, 1::2] = float("-inf")     # every other entry -inf, the sampled one finite
+        ids[b + 4] = 0
+        z[b + 5, :] = float("nan")         # masked: never read
+        mask[b + 5] = 0
+        ids[b + 6] = V                     # bad id on a valid row
+        ids[b + 7] = -1                    # bad id on a masked row
+        mask[b + 7] = 0
+        z[b + 8, 0] = float("inf")         # +inf at the row's start, sampled
+        ids[b + 8] = 0
+    lp_ref = torch.full((T,), -8.0, device=DEV)
+    lp_mu = lp_ref.clone()
+    adv = torch.linspace(-1, 1, T, device=DEV)
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), "mask_weight", "const", 1.0)
+    ref = run_oracle(z, ids, lp_mu, lp_ref, adv, mask, None, params)
+    for want in (True, False):
+        res = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, scale_mode="const",
+                                           want_dlogits=want)
+        torch.cuda.synchronize()
+        compare_loss(res, ref, params, dtype)
+        st = res.stats.cpu().numpy()
+        assert st[P.STAT_N_VALID] == T - 4 and st[P.STAT_N_BAD] == 2
+        assert math.isnan(res.loss.item()) and math.isnan(ref["loss"])
+    # the log-prob call reads every row, masked ones included
+    lp = P.logprob_fwd(z, ids)
+    torch.cuda.synchronize()
+    want_lp = oracle.logprob_fwd(_host_f64(z), ids.cpu().numpy())[0]
+    got = lp.cpu().double().numpy()
+    assert np.array_equal(np.isnan(got), np.isnan(want_lp))
+    assert_close_rel(got, want_lp, TIGHT, "log-prob call")
+
+
+def _host_f64(z):
+    if z.dtype == torch.bfloat16:
+        return oracle.bf16_bits_to_f64(z.cpu().view(torch.int16).numpy().view(np.uint16))
+    return z.cpu().double().numpy()
 
 
 def test_empty_batch():
