@@ -172,8 +172,15 @@ __device__ __forceinline__ void load16(uint32_t (&d)[4], __amdgpu_buffer_rsrc_t 
   d[2] = v.z;
   d[3] = v.w;
 }
+// A 16-byte store, then two wait states. On gfx950 a VALU write of a 16-byte buffer store's
+// data VGPRs issued right behind the store (seen: a v_mov_b64 into the first two) changed
+// the data being stored, and the compiler inserts no wait after a buffer store whose
+// offset is an SGPR. The scheduling barriers keep the wait directly behind the store.
 __device__ __forceinline__ void buf_store16_nt(u32x4 v, __amdgpu_buffer_rsrc_t r, int voff, int soff) {
   __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 1");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // Load of a value at a workgroup-uniform address through the scalar unit (constant

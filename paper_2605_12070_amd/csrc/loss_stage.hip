@@ -170,6 +170,29 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     const int64_t yy = uload(a.ids + rr);
     return yy >= 0 && yy < a.V;
   };
+  // The same decision in two halves (single-buffer kernels): the scalar loads it needs,
+  // issued at the top of a row for the next one (rr clamped into the batch), then the
+  // decision at the end of the row, when they have long arrived. A branch on a loaded value
+  // makes the wave wait for every scalar load in flight, so nothing branches on these
+  // before the end.
+  struct RowMeta {
+    uint32_t mword;   // the 32-bit word holding the mask byte (all ones without a mask)
+    int64_t y;
+  };
+  auto meta_load = [&](int64_t rr) -> RowMeta {
+    const int64_t q = rr < a.T ? rr : a.T - 1;
+    RowMeta m;
+    m.mword = (loss_mode && a.mask != nullptr)
+                  ? uload((const uint32_t*)(((uintptr_t)a.mask + (uintptr_t)q) & ~(uintptr_t)3))
+                  : 0xffffffffu;
+    m.y = uload(a.ids + q);
+    return m;
+  };
+  auto meta_reads = [&](int64_t rr, const RowMeta& m) -> bool {
+    if (!loss_mode) return true;
+    const uint32_t sh = 8u * (uint32_t)(((uintptr_t)a.mask + (uintptr_t)rr) & 3u);
+    return ((m.mword >> sh) & 0xffu) != 0 && m.y >= 0 && m.y < a.V;
+  };
   // Every load and store of the row goes through a buffer resource; a resource with
   // num_records = 0 turns an access into a no-op (loads read zeros, stores are dropped),
   // which keeps the chunk loops free of branches.
@@ -188,6 +211,8 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   uint32_t r2[DB ? NC : 1][4];             // the second row buffer (DB)
   StatCount sc;                            // thread 0's counters over this workgroup's rows
   int64_t row = blockIdx.x;
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
+  const float scale = loss_mode ? row_scale(a) : 1.0f;
   // Stagger the start of the workgroups that share an XCD: workgroups are dealt to the
   // eight XCDs in turn, so blockIdx / 8 numbers them within their XCD. Started together,
   // they would load, compute and store in lockstep and leave the XCD's memory path idle
@@ -202,6 +227,14 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     const __amdgpu_buffer_rsrc_t rz = load_rsrc(row, rd_cur);
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16<kAuxLast>(r1[c], rz, threadIdx.x * 16, c * NT * 16);
+  }
+  // Without DB the token id of a row comes with the metadata loaded a row ahead of it.
+  // It is waited for here: a load still in flight on entry would make the loop wait for every
+  // scalar load at the top of every row.
+  int64_t y_cur = 0;
+  if constexpr (!DB) {
+    y_cur = row < a.T ? uload(a.ids + row) : 0;
+    asm volatile("" :: "s"(y_cur));
   }
   int parity = 0;
   // One row: its chunks are in r (cur); nx receives the next row's chunks (nx is r itself
@@ -232,26 +265,33 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     auto ph_hi = [&](int c) { return ph + V - 8 * (c * NT + tid); };
 
     const int64_t next = row + gridDim.x;
-    const bool rd_next = next < a.T && reads(next);
-    const __amdgpu_buffer_rsrc_t rn = load_rsrc(rd_next ? next : row, rd_next);
+    // Without DB, the scalar loads are all issued here and waited for only where they are
+    // used, after the merge: the mask word and id of the next row (whose loads follow pass
+    // B), this row's token inputs and the word holding z[y] (its id came with the previous
+    // row's metadata); waiting for them at the top of the row took several scalar round
+    // trips per row (0.3 % of the large_vocab and long_agentic steps). DB issues the next
+    // row's loads here and decides first whether it is read (the look-ahead measured 2 %
+    // slower there).
+    const RowMeta mt = DB ? RowMeta{0u, 0} : meta_load(next);
+    bool rd_next = false;
+    int64_t y = y_cur;
     if constexpr (DB) {
+      rd_next = next < a.T && reads(next);
+      const __amdgpu_buffer_rsrc_t rn = load_rsrc(rd_next ? next : row, rd_next);
 #pragma unroll
       for (int c = 0; c < NC; ++c) load16<kAuxLast>(nx[c], rn, voff, c * NT * 16);
+      y = uload(a.ids + row);
     }
-    const int64_t y = uload(a.ids + row);
+    const TokenIn tin = token_inputs(a, row, scale);
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
-    const TokenIn tin = token_inputs(a, row);   // scalar loads, in flight during pass A
     float w = 0.0f, dy = 0.0f, l2 = 0.0f;
 
     if (rd_cur) {
-      // z[y] through the scalar unit (the aligned 32-bit word holding it). The row's bytes
-      // are written, in place, only by this workgroup and only after this read.
-      float zy = 0.0f;
-      if (good) {
-        const uintptr_t at = (uintptr_t)logits_of(a, row) + (uintptr_t)(row * a.ld + y) * 2u;
-        const uint32_t wv = uload((const uint32_t*)(at & ~(uintptr_t)3));
-        zy = (at & 2u) ? bf16_hi(wv) : bf16_lo(wv);
-      }
+      // z[y] through the scalar unit (the aligned 32-bit word holding it; a bad id reads the
+      // row's first word, unused), unpacked after the merge. The row's bytes are written,
+      // in place, only by this workgroup and only after this read.
+      const uintptr_t at = (uintptr_t)logits_of(a, row) + (uintptr_t)(row * a.ld + (good ? y : 0)) * 2u;
+      const uint32_t zword = uload((const uint32_t*)(at & ~(uintptr_t)3));
       // Pass A.
       float N = -INFINITY, S = 0.0f;
 #pragma unroll
@@ -299,6 +339,7 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
       parity ^= 1;                          // the buffers alternate between merges
       // An all -inf row has no finite shift: lse is NaN, as in IEEE max-shifted evaluation.
       const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
+      const float zy = good ? ((at & 2u) ? bf16_hi(zword) : bf16_lo(zword)) : 0.0f;
       finish_row(a, row, zy, lse2, good, &bc, tin, sc);
       if (want_d) {
         __syncthreads();
@@ -376,8 +417,11 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
     // memory counter retires in order, and loads queued behind interleaved stores would
     // make every wait in the next row's pass A also wait for store acknowledgements.
     if constexpr (!DB) {
+      rd_next = next < a.T && meta_reads(next, mt);
+      const __amdgpu_buffer_rsrc_t rn = load_rsrc(rd_next ? next : row, rd_next);
 #pragma unroll
       for (int c = 0; c < NC; ++c) load16<kAuxLast>(nx[c], rn, voff, c * NT * 16);
+      y_cur = mt.y;
     }
     if (want_d && !rd_cur) {                // zeros for a row that was not read
       const __amdgpu_buffer_rsrc_t rz = row_rsrc(dbase, dbytes);

@@ -27,8 +27,9 @@ struct TokenIn {
 
 __device__ __forceinline__ float row_scale(const RowArgs& a);
 
-// Inputs of the row a workgroup works on (uniform address: scalar loads).
-__device__ __forceinline__ TokenIn token_inputs(const RowArgs& a, int64_t row) {
+// Inputs of the row a workgroup works on (uniform address: scalar loads), with the call's
+// scale (row_scale, the same for every row) already known.
+__device__ __forceinline__ TokenIn token_inputs(const RowArgs& a, int64_t row, float scale) {
   TokenIn t;
   if (a.mode == kModeLogprob) {
     t.lp_ref = t.lp_mu = t.adv = 0.0f;
@@ -39,8 +40,11 @@ __device__ __forceinline__ TokenIn token_inputs(const RowArgs& a, int64_t row) {
   t.lp_mu = uload(a.lp_mu + row);
   t.adv = uload(a.adv + row);
   t.ts = a.tscale ? uload(a.tscale + row) : 1.0f;
-  t.scale = row_scale(a);
+  t.scale = scale;
   return t;
+}
+__device__ __forceinline__ TokenIn token_inputs(const RowArgs& a, int64_t row) {
+  return token_inputs(a, row, a.mode == kModeLogprob ? 1.0f : row_scale(a));
 }
 
 __device__ __forceinline__ TokenOut token_math(const RowArgs& a, const TokenIn& t, float zy,

@@ -15,7 +15,7 @@ import paper_2605_12070_amd as P
 from paper_2605_12070_amd import workloads as W
 
 from helpers import (TIGHT, assert_close_rel, bits_of, compare_loss, oracle_anchor,
-                     oracle_params, run_oracle, tie_mask)
+                     oracle_params, run_oracle, tie_mask, torch_anchor)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -355,17 +355,28 @@ def test_in_place_dlogits(dtype):
     assert torch.equal(in_place.logp, out_of_place.logp)
 
 
-def test_deterministic_bitwise():
-    wl = W.make_workload("small_vocab", device=DEV, T=1024, seed=11)
-    _say("determinism", wl.T, wl.V)
-    anchor = oracle_anchor(wl.logits, wl.ids).to(DEV)
+# two-buffer rows, the flagship shape with several rows per workgroup, masked rows, rows
+# with a phase
+@pytest.mark.parametrize("name,T,V", [("small_vocab", 1024, None), ("large_vocab", 600, None),
+                                      ("long_agentic", 600, None), ("small_vocab", 500, 151937)])
+def test_deterministic_bitwise(name, T, V):
+    """Three calls into dlogits buffers that start out as NaN and as zeros give the same bits:
+    no entry is left unwritten or written from registers that were still being stored."""
+    wl = W.make_workload(name, device=DEV, T=T, V=V, seed=11)
+    _say("determinism", name, wl.T, wl.V)
+    anchor = torch_anchor(wl.logits, wl.ids)
     lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
-    a = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv)
-    b = P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv)
-    torch.cuda.synchronize()
-    for x, y in ((a.loss, b.loss), (a.dlogits, b.dlogits), (a.logp, b.logp), (a.stats, b.stats),
-                 (a.loss_tok, b.loss_tok), (a.flags, b.flags)):
-        assert torch.equal(x, y)
+    runs = []
+    for fill in (float("nan"), 0.0, float("nan")):
+        d = torch.full_like(wl.logits, fill)
+        runs.append(P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, lp_ref, wl.adv,
+                                                 wl.mask, dlogits=d))
+        torch.cuda.synchronize()
+    a = runs[0]
+    for b in runs[1:]:
+        for x, y in ((a.loss, b.loss), (a.dlogits, b.dlogits), (a.logp, b.logp),
+                     (a.stats, b.stats), (a.loss_tok, b.loss_tok), (a.flags, b.flags)):
+            assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))
 
 
 def test_masked_rows_bad_ids_and_nonfinite_rows():
