@@ -17,6 +17,7 @@ import pytest
 
 from paper_2605_12070_amd import build as B
 
+
 def _vregs(tok):
     m = re.match(r"v\[(\d+):(\d+)\]$", tok)
     if m:
