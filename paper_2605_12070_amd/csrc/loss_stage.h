@@ -74,6 +74,9 @@ struct RowLaunch {
 };
 
 constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the prefix kernels
+// tail chunks per thread the fp32 prefix kernel also keeps in LDS (16 KB per unit at 1024
+// threads)
+constexpr int kPrefixKeepF32 = 9;
 
 // aligned: the rows (and dlogits rows) start on 16-byte boundaries. phase_ok: bf16 rows that
 // start anywhere (2-byte aligned), with dlogits (if any) at the logits' phase on every row;
