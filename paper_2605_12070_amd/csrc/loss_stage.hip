@@ -6,8 +6,12 @@
 // rows). A row of V = 151936 bf16 logits (297 KiB) is loaded once with 16-byte loads and
 // kept in registers (1024 threads x 19 x 16 B); the thread's exponentials replace the
 // logits in the same registers as fp16 pairs, so the backward sweep reads nothing from
-// memory and writes dlogits once with 16-byte non-temporal stores. Rows longer than the
-// register budget, or unaligned rows, use a streaming kernel that reads the row twice.
+// memory and writes dlogits once with 16-byte non-temporal stores. bf16 rows that start
+// anywhere or end in a partial chunk run in the same kernels with the neighbouring entries
+// masked (the phase kernels). Rows longer than the register budget keep a resident prefix
+// and read only the rest twice (the prefix kernels); what is left (fp32 rows off a 16-byte
+// boundary, forward calls on rows past the budget) uses a streaming kernel that reads the
+// row twice.
 #include "dppo.h"
 #include "dppo_device.h"
 #include "loss_stage.h"
