@@ -607,14 +607,25 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
   StatCount sc;
+  const bool loss_mode = a.mode != kModeLogprob;
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
+  const float scale = loss_mode ? row_scale(a) : 1.0f;
   // one row; the merge's second barrier orders the LDS reuse between consecutive rows
   auto one = [&](const int64_t row) {
     const int tid = threadIdx.x;
     const int V = a.V;
     const int nfull = V >> 2;
-    const bool loss_mode = a.mode != kModeLogprob;
-    const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
-    const int64_t y = a.ids[row];
+    // Every scalar load of the row is issued before the first branch on any of them (a
+    // branch on a loaded value waits for all scalar loads in flight), so they share one
+    // round trip; the token inputs are used after the merge. With one row per workgroup
+    // (a short batch) the chain of round trips was most of the kernel's time.
+    const uint32_t mword =
+        (loss_mode && a.mask != nullptr)
+            ? uload((const uint32_t*)(((uintptr_t)a.mask + (uintptr_t)row) & ~(uintptr_t)3))
+            : 0xffffffffu;
+    const int64_t y = uload(a.ids + row);
+    const TokenIn tin = token_inputs(a, row, scale);
+    const bool valid = ((mword >> (8u * (uint32_t)(((uintptr_t)a.mask + (uintptr_t)row) & 3u))) & 0xffu) != 0;
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
     if (loss_mode && !(valid && good)) {
       skip_row_resident<NT, NC, 4>(a, row, valid, sc);
@@ -680,7 +691,7 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
     block_merge_ns<NT>(n, s, red);
     const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
 
-    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    finish_row(a, row, zy, lse2, good, &bc, tin, sc);
     if (!BWD || !a.dlogits) return;
     __syncthreads();
     const float w = bc.w;
