@@ -808,14 +808,23 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgsOf<BWD> a) {
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
   StatCount sc;
+  const bool loss_mode = a.mode != kModeLogprob;
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
+  const float scale = loss_mode ? row_scale(a) : 1.0f;
   // one row; the merge's second barrier orders the LDS reuse between consecutive rows
   auto one = [&](const int64_t row) {
     const int tid = threadIdx.x;
     const int V = a.V;
     const int nchunk = (V + E - 1) / E;
-    const bool loss_mode = a.mode != kModeLogprob;
-    const bool valid = !loss_mode || a.mask == nullptr || a.mask[row] != 0;
-    const int64_t y = a.ids[row];
+    // the row's scalar loads, issued before the first branch on any of them (the token
+    // inputs are used after the merge)
+    const uint32_t mword =
+        (loss_mode && a.mask != nullptr)
+            ? uload((const uint32_t*)(((uintptr_t)a.mask + (uintptr_t)row) & ~(uintptr_t)3))
+            : 0xffffffffu;
+    const int64_t y = uload(a.ids + row);
+    const TokenIn tin = token_inputs(a, row, scale);
+    const bool valid = ((mword >> (8u * (uint32_t)(((uintptr_t)a.mask + (uintptr_t)row) & 3u))) & 0xffu) != 0;
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
     if (loss_mode && !(valid && good)) {
       skip_row<Tin, NT>(a, row, valid, sc);
@@ -841,7 +850,7 @@ __global__ __launch_bounds__(NT) void rows_stream(RowArgsOf<BWD> a) {
     block_merge_ns<NT>(n, s, red);
     const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
 
-    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    finish_row(a, row, zy, lse2, good, &bc, tin, sc);
     if (!BWD || !a.dlogits) return;
     __syncthreads();
     const float w = bc.w;
@@ -915,12 +924,17 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
   __shared__ Bcast bc;
   __shared__ u32x4 keep[KS * NT];
   StatCount sc;
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
+  const float scale = row_scale(a);
   for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
     const int tid = threadIdx.x;
     const int V = a.V;
     const int nfull = V >> 2;             // whole 16-byte chunks, > P by the selection
     const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
     const int64_t y = uload(a.ids + row);
+    // issued with the row's other scalar loads, before the first branch on them; used after
+    // the merge
+    const TokenIn tin = token_inputs(a, row, scale);
     const bool good = (y >= 0) && (y < V);
     if (!(valid && good)) {               // uniform
       skip_row_long<float, NT>(a, row, valid, sc);
@@ -997,7 +1011,7 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
     merge_ns(n, s, nt, st);
     block_merge_ns<NT>(n, s, red);
     const float lse2 = (n == -INFINITY) ? __builtin_nanf("") : n + log2f(s);
-    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    finish_row(a, row, zy, lse2, good, &bc, tin, sc);
     if (!a.dlogits) continue;             // uniform
     __syncthreads();
     const float w = bc.w;
@@ -1069,12 +1083,17 @@ __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
   __shared__ Bcast bc;
   __shared__ float nch[NC][NT];           // per-chunk shifts, [c][tid]: conflict-free
   StatCount sc;
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
+  const float scale = row_scale(a);
   for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
     const int tid = threadIdx.x;
     const int V = a.V;
     const int nfull = V >> 3;             // whole 16-byte chunks, >= P by the selection
     const bool valid = a.mask == nullptr || uload_u8(a.mask + row) != 0;
     const int64_t y = uload(a.ids + row);
+    // issued with the row's other scalar loads, before the first branch on them; used after
+    // the merge
+    const TokenIn tin = token_inputs(a, row, scale);
     const bool good = (y >= 0) && (y < V);
     if (!(valid && good)) {               // uniform
       skip_row_long<uint16_t, NT>(a, row, valid, sc);
@@ -1153,7 +1172,7 @@ __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
     merge_ns(N, S, nt, st);
     block_merge_ns<NT>(N, S, red);
     const float lse2 = (N == -INFINITY) ? __builtin_nanf("") : N + log2f(S);
-    finish_row(a, row, zy, lse2, good, &bc, token_inputs(a, row), sc);
+    finish_row(a, row, zy, lse2, good, &bc, tin, sc);
     if (!a.dlogits) continue;             // uniform
     __syncthreads();
     const float w = bc.w;
