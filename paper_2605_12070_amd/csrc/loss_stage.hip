@@ -956,7 +956,9 @@ __global__ __launch_bounds__(NT) void rows_f32_prefix(RowArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int idx = i0 + u * NT;
-        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+        // a chunk kept in LDS is read here for the last time (uniform condition)
+        if (s0 + u < KS) v[u] = buf_load16<kAuxLast>(rz, idx < nfull ? idx * 16 : kOff, 0);
+        else v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
