@@ -77,6 +77,8 @@ constexpr int kPrefixNC = 19;  // resident 16-byte chunks per thread of the pref
 // tail chunks per thread the fp32 prefix kernel also keeps in LDS (16 KB per unit at 1024
 // threads)
 constexpr int kPrefixKeepF32 = 9;
+// and the bf16 prefix kernel, beside its 76 KB shift table
+constexpr int kPrefixKeepBf16 = 5;
 
 // aligned: the rows (and dlogits rows) start on 16-byte boundaries. phase_ok: bf16 rows that
 // start anywhere (2-byte aligned), with dlogits (if any) at the logits' phase on every row;

@@ -1081,9 +1081,13 @@ template <int NT, int NC>
 __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
   constexpr int P = NT * NC;              // resident chunks of a row
   constexpr int U = 4;                    // tail chunks per thread in flight
+  // the first KS of each thread's tail chunks also wait in LDS between the passes (each
+  // thread reads back only what it wrote), beside the shift table
+  constexpr int KS = kPrefixKeepBf16;
   __shared__ float red[2 * (NT / 64) + 2];
   __shared__ Bcast bc;
   __shared__ float nch[NC][NT];           // per-chunk shifts, [c][tid]: conflict-free
+  __shared__ u32x4 keep[KS * NT];
   StatCount sc;
   // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
   const float scale = row_scale(a);
@@ -1111,12 +1115,18 @@ __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
     const bool rag_owner = (V & 7) != 0 && tid == nfull % NT;
     // pass A, tail: general (max, sum) partials per chunk
     float nt = -INFINITY, st = 0.0f;
-    for (int i0 = P + tid; i0 < nfull; i0 += U * NT) {
+    for (int i0 = P + tid, s0 = 0; i0 < nfull; i0 += U * NT, s0 += U) {
       u32x4 v[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int idx = i0 + u * NT;
-        v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+        // a chunk kept in LDS is read here for the last time (uniform condition)
+        if (s0 + u < KS) v[u] = buf_load16<kAuxLast>(rz, idx < nfull ? idx * 16 : kOff, 0);
+        else v[u] = buf_load16(rz, idx < nfull ? idx * 16 : kOff, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (s0 + u < KS) keep[(s0 + u) * NT + tid] = v[u];
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -1207,12 +1217,13 @@ __global__ __launch_bounds__(NT) void rows_bf16_prefix(RowArgs a) {
       buf_store16_nt(v, rd, tid * 16, c * NT * 16);
     }
     // pass B, tail: re-read, w 2^(z L - lse2), store (stores past the row are dropped)
-    for (int i0 = P + tid; i0 < nfull; i0 += U * NT) {
+    for (int i0 = P + tid, s0 = 0; i0 < nfull; i0 += U * NT, s0 += U) {
       u32x4 v[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int idx = i0 + u * NT;
-        v[u] = buf_load16<kAuxLast>(rz, idx < nfull ? idx * 16 : kOff, 0);
+        if (s0 + u < KS) v[u] = keep[(s0 + u) * NT + tid];
+        else v[u] = buf_load16<kAuxLast>(rz, idx < nfull ? idx * 16 : kOff, 0);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
