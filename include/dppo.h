@@ -428,9 +428,11 @@ dppo_status dppo_ppo_clip_ratio(const int32_t* stats, double* ratio);
 dppo_status dppo_reset_decision(const int32_t* stats, double tau, int32_t patience,
                                 int32_t* streak, double* rho, int32_t* fire);
 
-/* Row-kernel policy, a testing and benchmarking hook: 0 = automatic (the
- * register-resident kernel when the row fits, the two-pass streaming kernel otherwise),
- * 1 = always the streaming kernel. Process-global; any other value is INVALID_ARG. */
+/* Row-kernel policy, a testing and benchmarking hook, two bits. Bit 0: clear = automatic
+ * (the register-resident kernel when the row fits, the two-pass streaming kernel
+ * otherwise), set = always the streaming kernel. Bit 1: decoupled_ppo_loss_fwd_bwd counts
+ * its statistics with a counting kernel and atomics even where it would otherwise take them
+ * from the flags (same results). Process-global; a value outside 0..3 is INVALID_ARG. */
 dppo_status dppo_set_path_policy(int32_t policy);
 
 /* Name of the per-row kernel (as profilers print it) that a call with this logits dtype,

@@ -392,8 +392,10 @@ def ewma_proxy_update(x_prox: torch.Tensor, x_new: torch.Tensor, beta: float, w:
 
 
 def set_path_policy(policy: str):
-    """'auto' (register-resident rows when they fit) or 'stream' (always two-pass)."""
-    code = {"auto": 0, "stream": 1}[policy]
+    """'auto' (register-resident rows when they fit) or 'stream' (always two-pass); with
+    '+atomics' appended the loss call counts its statistics with its counting kernel and
+    atomics even where it would take them from the flags (a testing hook: same results)."""
+    code = {"auto": 0, "stream": 1, "auto+atomics": 2, "stream+atomics": 3}[policy]
     _lib.check(_lib.lib().dppo_set_path_policy(code), "dppo_set_path_policy")
 
 

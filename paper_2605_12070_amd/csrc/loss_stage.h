@@ -13,6 +13,8 @@ namespace dppo {
 constexpr int kModeLogprob = 0;  // log-prob (and lse) only
 constexpr int kModeLoss = 1;     // decoupled PPO loss, optional dlogits
 
+// Row-kernel policy (dppo_set_path_policy): bit 0 forces the streaming kernel; the ABI layer
+// also reads bit 1 (counters by prep_stats and atomics only).
 constexpr int kForceAuto = 0;
 constexpr int kForceStream = 1;  // use the two-pass streaming kernel even when resident fits
 
@@ -45,6 +47,10 @@ struct RowArgs {
   float alpha;          // behaviour-policy weight of an interpolated reference
   int32_t stagger;      // persistent bf16 kernels: start delay per XCD-local workgroup index,
                         // in s_sleep(6) units (set by the launcher from RowLaunch)
+  int32_t count_mode;   // 1 (persistent fp32 resident loss calls that write flags): no
+                        // prep_stats; each workgroup counts the valid tokens itself for the
+                        // token-mean scale (workgroup 0 stores the count), no counter
+                        // atomics; loss_sum derives the counters from the flags
 };
 
 // Arguments of the kernels without the backward sweep: the row arguments plus an optional
@@ -69,6 +75,7 @@ struct RowLaunch {
   bool two_buffers = false; // resident backward kernel with two row buffers
   bool prefix = false;       // backward kernel with a resident prefix and a streamed tail
   bool phase = false;        // bf16 resident kernel for rows with a phase (rows_bf16_*phase*)
+  bool counts = false;       // the kernel supports count mode (RowArgs::count_mode)
   int fill = 27;             // persistent grids: workgroups launched per 32 resident slots
   int stagger = 2;           // RowArgs::stagger for the kernels that stagger their starts
 };
@@ -86,8 +93,13 @@ constexpr int kPrefixKeepBf16 = 5;
 RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, int force,
                             bool phase_ok = false);
 void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream_t st);
+// With flags (a count-mode row kernel ran before), also stores the five counters derived
+// from the flags (rd_mode decides which tokens are active).
 void launch_loss_sum(const float* loss_tok, const uint8_t* mask, const float* tscale,
-                     const int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
-                     float* loss_out, hipStream_t st);
+                     int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
+                     float* loss_out, hipStream_t st, const uint8_t* flags = nullptr,
+                     int32_t rd_mode = 0);
+// Longest batch whose loss call may run in count mode (every workgroup reads the whole mask).
+constexpr int64_t kCountModeMaxT = 65536;
 
 }  // namespace dppo

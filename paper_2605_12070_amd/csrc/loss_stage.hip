@@ -51,6 +51,59 @@ __device__ __forceinline__ bool version_ok(const A& a, int64_t row) {
   return true;
 }
 
+// The call's loss scale (Eq. 2: the token-mean normaliser, or the constant), once per
+// workgroup; every thread calls it. Normally prep_stats has stored the valid-token count; in
+// count mode the workgroup counts the mask itself (workgroup 0 also stores the count, for
+// loss_sum), which saves that launch for a short batch. Only the fp32 resident kernel
+// takes this path: in the bf16 kernels the extra prologue cost 0.7 % of the flagship's time
+// with count mode off, and count mode gained nothing at small_vocab.
+template <int NT>
+__device__ float call_scale(const RowArgs& a) {
+  if (a.mode == kModeLogprob) return 1.0f;
+  if (!a.count_mode) return row_scale(a);
+  if (a.scale_mode != DPPO_SCALE_TOKEN_MEAN) return a.loss_scale;
+  __shared__ int part[NT / 64];
+  int cnt = 0;
+  if (a.mask != nullptr) {
+    // 16-byte chunks from the 16-byte boundary at or below the mask, four per thread in
+    // flight (T <= kCountModeMaxT); a byte counts when it lies in [mask, mask + T)
+    const uintptr_t m0 = (uintptr_t)a.mask;
+    const int ph = (int)(m0 & 15u);
+    const int nb = ph + a.T;
+    const __amdgpu_buffer_rsrc_t r = row_rsrc((const void*)(m0 - (uintptr_t)ph), nb);
+    const int nch = (nb + 15) >> 4;
+    for (int c0 = threadIdx.x; c0 < nch; c0 += 4 * NT) {
+      u32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + u * NT;
+        v[u] = buf_load16(r, c < nch ? c * 16 : 0x7fffff00, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int base = (c0 + u * NT) * 16;
+#pragma unroll
+        for (int b = 0; b < 16; ++b) {
+          const int pos = base + b;
+          const uint32_t byte = (v[u][b >> 2] >> (8 * (b & 3))) & 0xffu;
+          cnt += (byte != 0u) & (pos >= ph) & (pos < nb);
+        }
+      }
+    }
+  } else if (threadIdx.x == 0) {
+    cnt = a.T;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = cnt;
+  __syncthreads();
+  int n = 0;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) n += part[i];
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.stats[DPPO_STAT_N_VALID] = n;
+  return a.loss_scale / (float)(n > 1 ? n : 1);
+}
+
 // Rows that are not evaluated (loss mask 0, or a bad token id on a valid row).
 template <typename Tin, int NT>
 __device__ void skip_row(const RowArgs& a, int64_t row, bool valid, StatCount& sc) {
@@ -514,6 +567,8 @@ __device__ __forceinline__ void fwd_rows(const RowArgsV& a) {
     const int steps = (int)((blockIdx.x >> 3) & 31) * a.stagger;
     for (int i = 0; i < steps; ++i) __builtin_amdgcn_s_sleep(6);
   }
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
+  const float scale = loss_mode ? row_scale(a) : 1.0f;
   bool rd_cur = row < a.T && reads(row);
   {
     const __amdgpu_buffer_rsrc_t rz = load_rsrc(row, rd_cur);
@@ -535,7 +590,7 @@ __device__ __forceinline__ void fwd_rows(const RowArgsV& a) {
     const __amdgpu_buffer_rsrc_t rn = load_rsrc(rd_next ? next : row, rd_next);
     const int64_t y = uload(a.ids + row);
     const bool good = (y >= 0) && (y < V) && version_ok(a, row);
-    const TokenIn tin = token_inputs(a, row);
+    const TokenIn tin = token_inputs(a, row, scale);
     float zy = 0.0f;
     if (rd_cur && good) {
       const uintptr_t at = (uintptr_t)logits_of(a, row) + (uintptr_t)(row * a.ld + y) * 2u;
@@ -609,7 +664,7 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
   StatCount sc;
   const bool loss_mode = a.mode != kModeLogprob;
   // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
-  const float scale = loss_mode ? row_scale(a) : 1.0f;
+  const float scale = call_scale<NT>(a);
   // one row; the merge's second barrier orders the LDS reuse between consecutive rows
   auto one = [&](const int64_t row) {
     const int tid = threadIdx.x;
@@ -726,7 +781,8 @@ __global__ __launch_bounds__(NT) void rows_f32_resident(RowArgsOf<BWD> a) {
     }
   };
   for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) one(row);
-  if (threadIdx.x == 0) flush_stats(a, sc);
+  // in count mode the counters come from the flags (loss_sum)
+  if (threadIdx.x == 0 && !a.count_mode) flush_stats(a, sc);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -1281,23 +1337,30 @@ __global__ __launch_bounds__(1024) void prep_stats(const uint8_t* mask, int64_t 
 // L = sum_t m_t s_t l_t in float64, each thread over a fixed stride, then a fixed tree:
 // the same inputs give the same bits on every run.
 template <bool HAS_MASK, bool HAS_TSCALE>
+// With flags (count mode), the counters are derived from them as well: n_valid, n_band,
+// n_ppo, n_active (PPO-active, and in the band when rd_mode masks by it) and n_bad.
 __global__ __launch_bounds__(1024) void loss_sum(const float* loss_tok, const uint8_t* mask,
-                                                 const float* tscale, const int32_t* stats,
+                                                 const float* tscale, int32_t* stats,
                                                  int64_t T, float loss_scale, int32_t scale_mode,
-                                                 float* loss_out) {
+                                                 float* loss_out, const uint8_t* flags,
+                                                 int32_t rd_mode) {
   __shared__ double part[16];
+  __shared__ int cpart[16][5];
   float scale = loss_scale;
   if (scale_mode == DPPO_SCALE_TOKEN_MEAN) {
     const int n = stats[DPPO_STAT_N_VALID];
     scale = loss_scale / (float)(n > 1 ? n : 1);
   }
+  const bool uses_band = rd_mode == DPPO_RD_MASK || rd_mode == DPPO_RD_MASK_WEIGHT;
   // Thread k adds tokens k, k + 1024, k + 2048, ... in that order; the loads of 16 of them
   // are issued together so that their latencies overlap.
   constexpr int U = 16;
   double acc = 0.0;
+  int c[5] = {0, 0, 0, 0, 0};
   for (int64_t base = threadIdx.x; base < T; base += 1024 * U) {
     float lt[U], ts[U];
     bool on[U];
+    uint32_t fl[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t i = base + (int64_t)u * 1024;
@@ -1305,19 +1368,42 @@ __global__ __launch_bounds__(1024) void loss_sum(const float* loss_tok, const ui
       lt[u] = loss_tok[j];
       ts[u] = HAS_TSCALE ? tscale[j] : 1.0f;
       on[u] = (i < T) & ((HAS_MASK ? mask[j] : (uint8_t)1) != 0);
+      fl[u] = (flags != nullptr && i < T) ? flags[j] : 0u;
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
       if (on[u]) acc += (double)(scale * ts[u]) * (double)lt[u];
+      const bool band = fl[u] & DPPO_FLAG_BAND, ppo = fl[u] & DPPO_FLAG_PPO;
+      c[DPPO_STAT_N_VALID] += (fl[u] & DPPO_FLAG_VALID) != 0;
+      c[DPPO_STAT_N_BAND] += band;
+      c[DPPO_STAT_N_PPO] += ppo;
+      c[DPPO_STAT_N_ACTIVE] += ppo && (band || !uses_band);
+      c[DPPO_STAT_N_BAD] += (fl[u] & DPPO_FLAG_BAD_ID) != 0;
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+#pragma unroll
+  for (int k = 0; k < 5; ++k)
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) c[k] += __shfl_xor(c[k], off, 64);
+  if ((threadIdx.x & 63) == 0) {
+    part[threadIdx.x >> 6] = acc;
+#pragma unroll
+    for (int k = 0; k < 5; ++k) cpart[threadIdx.x >> 6][k] = c[k];
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     double tot = 0.0;
     for (int i = 0; i < 16; ++i) tot += part[i];
     loss_out[0] = (float)tot;
+    if (flags != nullptr) {
+      for (int k = 0; k < 5; ++k) {
+        int n = 0;
+        for (int i = 0; i < 16; ++i) n += cpart[i][k];
+        stats[k] = n;
+      }
+    }
   }
 }
 
@@ -1481,7 +1567,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   // fp32 rows on an aligned stride may end in a partial chunk: rows_f32_resident loads and
   // stores its last V % 4 entries one by one
   const bool f32_ragged = dtype == DPPO_F32 && aligned && !whole_chunks;
-  if (((aligned && whole_chunks) || ph || f32_ragged) && force != kForceStream) {
+  if (((aligned && whole_chunks) || ph || f32_ragged) && !(force & kForceStream)) {
     for (int i = 0; i < kNumResident; ++i) {
       if ((int64_t)kResident[i].nt * kResident[i].nc >= chunks) {
         pick = i;
@@ -1502,6 +1588,8 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
                         : pick_bf16_fwd(pick))
                  : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
     L.two_buffers = dtype == DPPO_BF16 && bwd && kResidentDB[pick];
+    // the fp32 resident kernel can count the valid tokens itself (count mode)
+    L.counts = dtype == DPPO_F32;
     L.resident = true;
     // fp32 forward rows loop persistently at every shape: 0-2.5 % faster than one workgroup
     // per row for 1024 x 6 .. 12 (the gradient kernel there is 0-6 % slower persistent)
@@ -1513,7 +1601,7 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
   }
   L.threads = 1024;
   L.resident = false;
-  if (bwd && aligned && force != kForceStream && (V * esize) / 16 >= (int64_t)1024 * kPrefixNC) {
+  if (bwd && aligned && !(force & kForceStream) && (V * esize) / 16 >= (int64_t)1024 * kPrefixNC) {
     // longer rows: a resident prefix of 1024 x kPrefixNC whole chunks, the rest (and a
     // ragged end) streamed twice
     L.fn = dtype == DPPO_F32 ? (const void*)rows_f32_prefix<1024, kPrefixNC>
@@ -1543,11 +1631,12 @@ void launch_prep_stats(const uint8_t* mask, int64_t T, int32_t* stats, hipStream
 }
 
 void launch_loss_sum(const float* loss_tok, const uint8_t* mask, const float* tscale,
-                     const int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
-                     float* loss_out, hipStream_t st) {
+                     int32_t* stats, int64_t T, float loss_scale, int32_t scale_mode,
+                     float* loss_out, hipStream_t st, const uint8_t* flags, int32_t rd_mode) {
   auto k = mask ? (tscale ? loss_sum<true, true> : loss_sum<true, false>)
                 : (tscale ? loss_sum<false, true> : loss_sum<false, false>);
-  k<<<1, 1024, 0, st>>>(loss_tok, mask, tscale, stats, T, loss_scale, scale_mode, loss_out);
+  k<<<1, 1024, 0, st>>>(loss_tok, mask, tscale, stats, T, loss_scale, scale_mode, loss_out,
+                        flags, rd_mode);
 }
 
 }  // namespace dppo

@@ -196,8 +196,10 @@ def test_ewma_empty_buffer_updates_w_only():
 
 def test_path_policy_validation():
     L = _lib.lib()
-    assert L.dppo_set_path_policy(2) == _lib.DPPO_ERR_INVALID_ARG
-    assert L.dppo_set_path_policy(0) == _lib.DPPO_OK
+    for bad in (-1, 4, 7):
+        assert L.dppo_set_path_policy(bad) == _lib.DPPO_ERR_INVALID_ARG
+    for ok in (3, 2, 1, 0):
+        assert L.dppo_set_path_policy(ok) == _lib.DPPO_OK
 
 
 def test_timer_read_requires_outputs():

@@ -379,6 +379,50 @@ def test_deterministic_bitwise(name, T, V):
             assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))
 
 
+# loss calls with the counters taken from the flags (count mode: the fp32 resident kernel)
+# or counted by the kernels (every other family), against the same calls forced to count with
+# the counting kernel and atomics
+@pytest.mark.parametrize("name,T,V,rd_mode,scale_mode,bwd", [
+    ("tiny", 256, None, "mask", "token_mean", True),
+    ("small_vocab", 3000, None, "weight", "token_mean", True),
+    ("large_vocab", 400, None, "mask_weight", "const", True),
+    ("long_agentic", 700, 30000, "mask_weight", "token_mean", True),
+    ("long_agentic", 700, 30000, "none", "token_mean", False),
+    ("small_vocab", 500, 151937, "mask", "token_mean", True),
+    ("long_agentic", 200, 262144, "mask_weight", "token_mean", True),
+    ("tiny", 300, 151936, "mask_weight", "token_mean", True),
+])
+def test_counters_from_flags_equal_atomic_counters(name, T, V, rd_mode, scale_mode, bwd):
+    wl = W.make_workload(name, device=DEV, T=T, V=V, seed=23)
+    _say("count mode", name, wl.T, wl.V, rd_mode, scale_mode, bwd)
+    anchor = torch_anchor(wl.logits, wl.ids)
+    lp_ref, lp_mu = W.reference_logprobs(anchor, wl)
+    ids = wl.ids.clone()
+    ids[7] = wl.V + 3                                  # a bad id on a (probably) valid row
+    res = {}
+    for policy in ("auto", "auto+atomics"):
+        P.set_path_policy(policy)
+        try:
+            out = None
+            for _ in range(2):                         # stale outputs must not leak
+                out = P.decoupled_ppo_loss_fwd_bwd(wl.logits, ids, lp_mu, lp_ref, wl.adv, wl.mask,
+                                                   rd_mode=rd_mode, scale_mode=scale_mode,
+                                                   loss_scale=0.5, want_dlogits=bwd, out=out)
+            torch.cuda.synchronize()
+        finally:
+            P.set_path_policy("auto")
+        res[policy] = out
+    a, b = res["auto"], res["auto+atomics"]
+    for x, y in ((a.stats, b.stats), (a.loss, b.loss), (a.logp, b.logp), (a.loss_tok, b.loss_tok),
+                 (a.flags, b.flags)) + (((a.dlogits, b.dlogits),) if bwd else ()):
+        assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))
+    st = a.stats.cpu().numpy()
+    mask = wl.mask.cpu().numpy()
+    assert st[P.STAT_N_VALID] == int((mask != 0).sum())
+    params = oracle_params((0.5, 2.0), (0.2, 0.2), rd_mode, scale_mode, 0.5)
+    np.testing.assert_array_equal(st, oracle.stats_of(a.flags.cpu().numpy(), params))
+
+
 def test_masked_rows_bad_ids_and_nonfinite_rows():
     T, V = 10, 3000
     _say("edge rows", T, V)
