@@ -104,16 +104,11 @@ __global__ __launch_bounds__(256) void ewma_kernel_scalar_dev(void* xp_, const v
 }
 
 // The reset rule (Sec. 5.2, App. E) and the coefficients of the recursion (App. B), in
-// double as the host path computes them: one thread.
-__global__ __launch_bounds__(64) void ewma_controller(const int32_t* stats, dppo_ewma_state* s,
-                                                      float beta, double tau, int32_t patience,
-                                                      int32_t normalized) {
-  if (threadIdx.x != 0) return;
-  dppo_ewma_state st = *s;
-  if (normalized && !(__builtin_isfinite(st.w) && st.w >= 0.0)) {
-    s->error = 1;
-    return;
-  }
+// double as the host path computes them, from the state before the step to the state after
+// it. False when w is negative or not finite (the step then changes nothing but `error`).
+__device__ bool controller_step(const int32_t* stats, dppo_ewma_state& st, float beta,
+                                double tau, int32_t patience, int32_t normalized) {
+  if (normalized && !(__builtin_isfinite(st.w) && st.w >= 0.0)) return false;
   double rho = 1.0;
   bool fire = false;
   if (stats != nullptr) {
@@ -128,7 +123,55 @@ __global__ __launch_bounds__(64) void ewma_controller(const int32_t* stats, dppo
   st.last_rho = (float)rho;
   st.ca = (float)ca;
   st.cb = (float)cb;
-  *s = st;
+  return true;
+}
+
+// The controller alone, one thread; the element kernel follows on the stream.
+__global__ __launch_bounds__(64) void ewma_controller(const int32_t* stats, dppo_ewma_state* s,
+                                                      float beta, double tau, int32_t patience,
+                                                      int32_t normalized) {
+  if (threadIdx.x != 0) return;
+  dppo_ewma_state st = *s;
+  if (controller_step(stats, st, beta, tau, patience, normalized)) *s = st;
+  else s->error = 1;
+}
+
+// Controller and update in one workgroup, for a buffer of at most kStepOneGroup elements
+// (a per-token proxy): thread 0 runs the controller and stores the new state (no other
+// workgroup reads it), then the workgroup applies the coefficients, four 16-byte vectors
+// (or elements) per thread in flight.
+template <bool BF16, bool VEC>
+__global__ __launch_bounds__(1024) void ewma_step_group(void* xp_, const void* xn_, int64_t n,
+                                                        const int32_t* stats,
+                                                        dppo_ewma_state* s, float beta,
+                                                        double tau, int32_t patience,
+                                                        int32_t normalized) {
+  __shared__ float coef[2];
+  __shared__ int ok;
+  if (threadIdx.x == 0) {
+    dppo_ewma_state st = *s;
+    const bool good = controller_step(stats, st, beta, tau, patience, normalized);
+    if (good) *s = st;
+    else s->error = 1;
+    coef[0] = st.ca;
+    coef[1] = st.cb;
+    ok = good;
+  }
+  __syncthreads();
+  if (!ok) return;
+  const float ca = coef[0], cb = coef[1];
+  constexpr int E = VEC ? (BF16 ? 8 : 4) : 1;
+  const int64_t work = n / E + n % E;     // vector threads, then one per tail element
+  for (int64_t i0 = threadIdx.x; i0 < work; i0 += 4 * 1024) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t i = i0 + (int64_t)u * 1024;
+      if (i < work) {
+        if (VEC) ewma_vec<BF16>(xp_, xn_, n, i, ca, cb, cb != 0.0f);
+        else ewma_elem<BF16>(xp_, xn_, i, ca, cb, cb != 0.0f);
+      }
+    }
+  }
 }
 
 hipError_t launch_ewma(void* xp, const void* xn, bool bf16, int64_t n, float ca, float cb,
@@ -164,8 +207,18 @@ hipError_t launch_ewma(void* xp, const void* xn, bool bf16, int64_t n, float ca,
 hipError_t launch_ewma_step(void* xp, const void* xn, bool bf16, int64_t n, float beta,
                             double tau, int32_t patience, bool normalized, const int32_t* stats,
                             dppo_ewma_state* state, bool aligned, hipStream_t st) {
+  if (n <= kStepOneGroup) {               // one launch for a small buffer
+    const int32_t nz = normalized ? 1 : 0;
+    if (aligned) {
+      if (bf16) ewma_step_group<true, true><<<1, 1024, 0, st>>>(xp, xn, n, stats, state, beta, tau, patience, nz);
+      else ewma_step_group<false, true><<<1, 1024, 0, st>>>(xp, xn, n, stats, state, beta, tau, patience, nz);
+    } else {
+      if (bf16) ewma_step_group<true, false><<<1, 1024, 0, st>>>(xp, xn, n, stats, state, beta, tau, patience, nz);
+      else ewma_step_group<false, false><<<1, 1024, 0, st>>>(xp, xn, n, stats, state, beta, tau, patience, nz);
+    }
+    return hipGetLastError();
+  }
   ewma_controller<<<1, 64, 0, st>>>(stats, state, beta, tau, patience, normalized ? 1 : 0);
-  if (n == 0) return hipGetLastError();
   const int64_t E = aligned ? (bf16 ? 8 : 4) : 1;
   const int64_t threads = n / E + n % E;
   const int64_t blocks = (threads + 255) / 256;

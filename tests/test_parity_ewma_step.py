@@ -35,8 +35,10 @@ def _rho_of(st):
     return 1.0 if st[0] == 0 else st[3] / st[0]
 
 
-# a buffer of a few workgroups and one of several hundred
-@pytest.mark.parametrize("n", [4099, 140003])
+# buffers the one-workgroup step takes (controller and update in one launch; 4099 with a
+# tail past its 16-byte vectors) and one of several hundred workgroups (the controller
+# kernel, then the element kernel)
+@pytest.mark.parametrize("n", [1001, 4099, 140003])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("normalized", [True, False])
 @pytest.mark.parametrize("patience", [1, 2])
@@ -112,9 +114,9 @@ def test_device_step_bad_normaliser_leaves_everything_unchanged(n):
     np.testing.assert_allclose(bits_of(dev.x), ref, rtol=2e-6, atol=2e-6)
 
 
+@pytest.mark.parametrize("n", [1001, 4099])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_device_step_unaligned_and_empty(dtype):
-    n = 4099
+def test_device_step_unaligned_and_empty(dtype, n):
     _say("ewma step unaligned", dtype, n)
     g = torch.Generator(device=DEV).manual_seed(9)
     xb = torch.randn(n + 1, generator=g, device=DEV).to(dtype)
