@@ -380,7 +380,8 @@ typedef struct {
  * ewma_proxy_step -- the reset controller and the PPO-EWMA update of ewma_proxy_update,
  * both on the device, so that a training step needs no device-to-host copy and no
  * synchronisation (the reset rule of Sec. 5.2 and App. E; the recursion of Eq. 5 / App. B).
- * A one-thread kernel reads the loss stage's counters and updates *state:
+ * The controller (one thread; for n <= 16384 in the same one-workgroup launch as the
+ * update) reads the loss stage's counters and updates *state:
  *    rho_t = n_active / n_valid (1 when n_valid = 0);
  *    streak <- streak + 1 if rho_t < tau (compared in double), else 0;
  *    a reset fires when streak >= patience; the streak then restarts at 0;
@@ -388,9 +389,9 @@ typedef struct {
  *    same rule on the host)
  *    w_t and (ca, cb) exactly as ewma_proxy_update computes them on the host, in double,
  *    then rounded to float.
- * The element kernel then applies x_prox <- ca x_new + cb x_prox (x_prox not read when
- * cb = 0) with the arithmetic of ewma_proxy_update, so both entry points give bit-identical
- * buffers for the same sequence of reset decisions.
+ * The update then applies x_prox <- ca x_new + cb x_prox (x_prox not read when cb = 0) with
+ * the arithmetic of ewma_proxy_update, so both entry points give bit-identical buffers for
+ * the same sequence of reset decisions.
  *  x_prox, x_new  [n] device buffers of `dtype`, as for ewma_proxy_update.
  *  beta           in [0, 1); tau finite; patience >= 1.
  *  stats          device [5] int32 counters of the step (decoupled_ppo_loss_fwd_bwd's
