@@ -36,9 +36,9 @@ def _rho_of(st):
 
 
 # buffers the one-workgroup step takes (controller and update in one launch; 4099 with a
-# tail past its 16-byte vectors) and one of several hundred workgroups (the controller
-# kernel, then the element kernel)
-@pytest.mark.parametrize("n", [1001, 4099, 140003])
+# tail past its 16-byte vectors; 16384 its largest) and ones of several workgroups (the
+# controller kernel, then the element kernel; 16385 the smallest)
+@pytest.mark.parametrize("n", [1001, 4099, 16384, 16385, 140003])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("normalized", [True, False])
 @pytest.mark.parametrize("patience", [1, 2])
