@@ -70,7 +70,11 @@ __device__ float call_scale(const RowArgs& a) {
     const uintptr_t m0 = (uintptr_t)a.mask;
     const int ph = (int)(m0 & 15u);
     const int nb = ph + a.T;
-    const __amdgpu_buffer_rsrc_t r = row_rsrc((const void*)(m0 - (uintptr_t)ph), nb);
+    // The range check drops a 4-byte word that reaches past the resource's end, so the
+    // resource runs to the next 4-byte boundary (readable, see the mask's requirement in the
+    // ABI); bytes past the mask are not counted.
+    const __amdgpu_buffer_rsrc_t r =
+        row_rsrc((const void*)(m0 - (uintptr_t)ph), (nb + 3) & ~3);
     const int nch = (nb + 15) >> 4;
     for (int c0 = threadIdx.x; c0 < nch; c0 += 4 * NT) {
       u32x4 v[4];

@@ -423,6 +423,36 @@ def test_counters_from_flags_equal_atomic_counters(name, T, V, rd_mode, scale_mo
     np.testing.assert_array_equal(st, oracle.stats_of(a.flags.cpu().numpy(), params))
 
 
+@pytest.mark.parametrize("off", [0, 1, 3, 13])
+def test_count_mode_mask_at_any_offset(off):
+    """The fp32 resident kernel counts the mask from the 16-byte boundary below it: a mask at
+    any byte offset gives the counts and scale of the counting kernel."""
+    T, V = 3001, 2000
+    _say("count mode mask offset", off, T, V)
+    g = torch.Generator(device=DEV).manual_seed(41 + off)
+    z = 2.0 * torch.randn(T, V, generator=g, device=DEV)
+    ids = torch.randint(0, V, (T,), generator=g, device=DEV)
+    mbuf = (torch.rand(T + 16, generator=g, device=DEV) > 0.3).to(torch.uint8)
+    mbuf[:off] = 7                                   # bytes before the mask must not count
+    mbuf[off + T:] = 9                               # nor bytes after it
+    mask = mbuf[off:off + T]
+    lp_ref = torch.full((T,), -7.0, device=DEV) + 0.1 * torch.randn(T, generator=g, device=DEV)
+    lp_mu = lp_ref + 0.05 * torch.randn(T, generator=g, device=DEV)
+    adv = torch.randn(T, generator=g, device=DEV)
+    res = {}
+    for policy in ("auto", "auto+atomics"):
+        P.set_path_policy(policy)
+        try:
+            res[policy] = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask)
+            torch.cuda.synchronize()
+        finally:
+            P.set_path_policy("auto")
+    a, b = res["auto"], res["auto+atomics"]
+    for x, y in ((a.stats, b.stats), (a.loss, b.loss), (a.dlogits, b.dlogits), (a.logp, b.logp)):
+        assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))
+    assert a.stats[P.STAT_N_VALID].item() == int(mask.sum().item())
+
+
 def test_masked_rows_bad_ids_and_nonfinite_rows():
     T, V = 10, 3000
     _say("edge rows", T, V)
