@@ -20,9 +20,11 @@
  *    dppo_last_error() then describes the failure. A launch failure returns DPPO_ERR_HIP.
  *    Nothing throws across the ABI.
  *  - Data errors are reported on the device, not in the return code (see below).
- *  - A loss mask ([T] uint8, where a call takes one) is read in aligned 4-byte words, so
- *    its allocation must be readable up to the next 4-byte boundary past mask + T (true of
- *    any hipMalloc or PyTorch allocation); the bytes past mask + T are ignored.
+ *  - A loss mask ([T] uint8, where a call takes one) is read in aligned 4-byte words (and,
+ *    to count its tokens, in the aligned 16-byte chunks that cover it), so its allocation
+ *    must be readable from the 16-byte boundary at or below mask up to the next 4-byte
+ *    boundary past mask + T (true of any hipMalloc or PyTorch allocation, and of views into
+ *    one); the bytes outside [mask, mask + T) are ignored.
  *  - Row strides (`ld`, `ld_dlogits`) are in elements. bf16 rows that do not start on a
  *    16-byte boundary, or whose length is not a multiple of 8, are read as the aligned
  *    16-byte chunks that cover them: the logits allocation must be readable from the 16-byte
