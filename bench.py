@@ -258,6 +258,38 @@ def vocab_shard_measure(dev, wl, lp_mu, lp_ref, n_shards=8, reps=20):
             "tokens_per_s": round(T / ((c_stats + c_loss) * 1e-3), 1)}
 
 
+def interpolated_reference_measure(dev, wl, lp_mu, dlogits, b_alg, reps=20):
+    """The fused call with the reference interpolated between mu_old and the current policy
+    (App. A: log-linear and arithmetic proxies, alpha = 0.5) on the large_vocab batch, the
+    reference formed per token inside the row kernel. Same algorithmic bytes as the main call
+    less the reference log-prob it no longer reads (4 B per token)."""
+    res = {}
+    for mode in ("log_linear", "linear"):
+        def call():
+            return P.decoupled_ppo_loss_fwd_bwd(wl.logits, wl.ids, lp_mu, None, wl.adv, wl.mask,
+                                                dlogits=dlogits, ref_mode=mode, alpha=0.5)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with P.KernelTimer() as kt:
+            e0.record(stream)
+            for _ in range(reps):
+                call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            k_ms, k_n = kt.read()
+        ms = k_ms / max(1, k_n)
+        b = b_alg - 4 * wl.T
+        gbps = b / (ms * 1e-3) / 1e9
+        res[mode] = {"kernel_ms": round(ms, 4), "achieved": round(gbps, 1),
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4), "alg_bytes_per_launch": b,
+                     "call_ms": round(e0.elapsed_time(e1) / reps, 4)}
+    return {"bound": "hbm", "peak": HBM_PEAK_GBPS, "unit": "GB/s", "alpha": 0.5,
+            "kernel": P.row_kernel_name(wl.logits.dtype, wl.V), **res}
+
+
 def long_rows_measure(dev, dtype=torch.float32, T=8192, V=151936, reps=10, key="fp32_rows"):
     """Rows longer than the register-resident kernels hold (fp32 past 77824 entries, bf16 past
     155648): N(0, 3^2) logits of `dtype`, uniform token ids, every token valid, the fused
@@ -419,6 +451,8 @@ def main():
                     help="skip the fused LM-head measurement")
     ap.add_argument("--no-shard", action="store_true",
                     help="skip the vocabulary-shard measurement")
+    ap.add_argument("--no-interp", action="store_true",
+                    help="skip the fused call with interpolated references (large_vocab only)")
     ap.add_argument("--no-versioned", action="store_true",
                     help="skip the versioned log-prob measurement")
     ap.add_argument("--no-fp32", action="store_true",
@@ -507,6 +541,10 @@ def main():
     if not args.no_shard and args.workload == "large_vocab":
         log("vocabulary shard")
         result["vocab_shard_roofline"] = vocab_shard_measure(dev, wl, lp_mu, lp_ref)
+    if not args.no_interp and args.workload == "large_vocab":
+        log("interpolated references")
+        result["interp_reference_roofline"] = interpolated_reference_measure(
+            dev, wl, lp_mu, dlogits, b_alg)
     if not args.no_versioned:
         log("versioned log-prob")
         del dlogits
