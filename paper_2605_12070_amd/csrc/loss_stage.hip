@@ -272,8 +272,9 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   uint32_t r2[DB ? NC : 1][4];             // the second row buffer (DB)
   StatCount sc;                            // thread 0's counters over this workgroup's rows
   int64_t row = blockIdx.x;
-  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs)
-  const float scale = loss_mode ? row_scale(a) : 1.0f;
+  // the call's scale (token-mean: from the valid-token count, fixed while the kernel runs);
+  // DB kernels take it after the first row's loads are issued (see below)
+  const float scale_top = (!DB && loss_mode) ? row_scale(a) : 1.0f;
   // Stagger the start of the workgroups that share an XCD: workgroups are dealt to the
   // eight XCDs in turn, so blockIdx / 8 numbers them within their XCD. Started together,
   // they would load, compute and store in lockstep and leave the XCD's memory path idle
@@ -289,6 +290,10 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) load16<kAuxLast>(r1[c], rz, threadIdx.x * 16, c * NT * 16);
   }
+  // In count mode the workgroup counts the mask here, its loads in flight together with the
+  // first row's: one memory round trip for both, where a counting kernel before this one
+  // costs a launch.
+  const float scale = DB ? call_scale<NT>(a) : scale_top;
   // Without DB the token id of a row comes with the metadata loaded a row ahead of it.
   // It is waited for here: a load still in flight on entry would make the loop wait for every
   // scalar load at the top of every row.
@@ -512,7 +517,8 @@ __device__ __forceinline__ void resident_rows(const RowArgsOf<BWD>& a) {
   } else {
     for (; row < a.T; row += gridDim.x) step(r1, r1, false);
   }
-  if (threadIdx.x == 0) flush_stats(a, sc);
+  // count mode: loss_sum derives the counters from the flags
+  if (threadIdx.x == 0 && !(DB && a.count_mode)) flush_stats(a, sc);
 }
 
 template <int NT, int NC, bool BWD>
@@ -1592,8 +1598,9 @@ RowLaunch select_row_kernel(int32_t dtype, int64_t V, bool aligned, bool bwd, in
                         : pick_bf16_fwd(pick))
                  : (bwd ? pick_f32<true>(pick) : pick_f32<false>(pick));
     L.two_buffers = dtype == DPPO_BF16 && bwd && kResidentDB[pick];
-    // the fp32 resident kernel can count the valid tokens itself (count mode)
-    L.counts = dtype == DPPO_F32;
+    // the fp32 resident kernel and the bf16 two-buffer kernels can count the valid tokens
+    // themselves (count mode)
+    L.counts = dtype == DPPO_F32 || L.two_buffers;
     L.resident = true;
     // fp32 forward rows loop persistently at every shape: 0-2.5 % faster than one workgroup
     // per row for 1024 x 6 .. 12 (the gradient kernel there is 0-6 % slower persistent)

@@ -423,14 +423,29 @@ def test_counters_from_flags_equal_atomic_counters(name, T, V, rd_mode, scale_mo
     np.testing.assert_array_equal(st, oracle.stats_of(a.flags.cpu().numpy(), params))
 
 
+COUNT_KINDS = {  # logits dtype, V, row stride, the kernel expected (count mode)
+    "f32": (torch.float32, 2000, 2000, "rows_f32_resident"),
+    "bf16": (torch.bfloat16, 32000, 32000, "rows_bf16_resident_db"),
+    "bf16_phase": (torch.bfloat16, 32000, 32001, "rows_bf16_phase_db"),
+}
+
+
+@pytest.mark.parametrize("kind", sorted(COUNT_KINDS))
 @pytest.mark.parametrize("off", [0, 1, 3, 13])
-def test_count_mode_mask_at_any_offset(off):
-    """The fp32 resident kernel counts the mask from the 16-byte boundary below it: a mask at
-    any byte offset gives the counts and scale of the counting kernel."""
-    T, V = 3001, 2000
-    _say("count mode mask offset", off, T, V)
+def test_count_mode_mask_at_any_offset(kind, off):
+    """The kernels that count the mask themselves (fp32 resident, bf16 with two row buffers)
+    read it from the 16-byte boundary below it: a mask at any byte offset gives the counts,
+    scale and outputs of the counting kernel, bit for bit."""
+    dtype, V, ld, kname = COUNT_KINDS[kind]
+    T = 3001
+    _say("count mode mask offset", kind, off, T, V, ld)
+    assert kname in P.row_kernel_name(dtype, V, ld)
     g = torch.Generator(device=DEV).manual_seed(41 + off)
-    z = 2.0 * torch.randn(T, V, generator=g, device=DEV)
+    zbuf = (2.0 * torch.randn(T * ld + 8, generator=g, device=DEV)).to(dtype)
+    z0 = 1 if ld != V else 0                         # the phase case starts off a 16-byte boundary
+    z = zbuf[z0:z0 + T * ld].view(T, ld)[:, :V]
+    dbuf = torch.zeros_like(zbuf)
+    dl = dbuf[z0:z0 + T * ld].view(T, ld)[:, :V]     # dlogits in the logits' layout
     ids = torch.randint(0, V, (T,), generator=g, device=DEV)
     mbuf = (torch.rand(T + 16, generator=g, device=DEV) > 0.3).to(torch.uint8)
     mbuf[:off] = 7                                   # bytes before the mask must not count
@@ -443,12 +458,14 @@ def test_count_mode_mask_at_any_offset(off):
     for policy in ("auto", "auto+atomics"):
         P.set_path_policy(policy)
         try:
-            res[policy] = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask)
+            r = P.decoupled_ppo_loss_fwd_bwd(z, ids, lp_mu, lp_ref, adv, mask, dlogits=dl)
             torch.cuda.synchronize()
+            res[policy] = (r, dl.clone())
         finally:
             P.set_path_policy("auto")
-    a, b = res["auto"], res["auto+atomics"]
-    for x, y in ((a.stats, b.stats), (a.loss, b.loss), (a.dlogits, b.dlogits), (a.logp, b.logp)):
+    (a, da), (b, db) = res["auto"], res["auto+atomics"]
+    for x, y in ((a.stats, b.stats), (a.loss, b.loss), (da, db), (a.logp, b.logp),
+                 (a.loss_tok, b.loss_tok), (a.flags, b.flags)):
         assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))
     assert a.stats[P.STAT_N_VALID].item() == int(mask.sum().item())
 
