@@ -14,7 +14,9 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
 
-@pytest.mark.parametrize("name,T", [("small_vocab", 1024), ("large_vocab", 512)])
+# tiny and small_vocab take count mode (the row kernel counts the mask), large_vocab the
+# counting kernel and atomics
+@pytest.mark.parametrize("name,T", [("tiny", 256), ("small_vocab", 1024), ("large_vocab", 512)])
 def test_captured_step_replays_match_eager(name, T):
     print(f"[case] graph capture {name} T={T}", flush=True)
     wl = W.make_workload(name, device=DEV, T=T)
@@ -55,6 +57,7 @@ def test_captured_step_replays_match_eager(name, T):
         proxy.state.copy_(before[1])
         dl.fill_(float("nan"))
         out.loss.fill_(float("nan"))
+        out.stats.fill_(-1)                      # every counter must be rewritten
         g.replay()
         torch.cuda.synchronize()
         got = snapshot()
