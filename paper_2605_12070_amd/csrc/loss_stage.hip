@@ -54,9 +54,11 @@ __device__ __forceinline__ bool version_ok(const A& a, int64_t row) {
 // The call's loss scale (Eq. 2: the token-mean normaliser, or the constant), once per
 // workgroup; every thread calls it. Normally prep_stats has stored the valid-token count; in
 // count mode the workgroup counts the mask itself (workgroup 0 also stores the count, for
-// loss_sum), which saves that launch for a short batch. Only the fp32 resident kernel
-// takes this path: in the bf16 kernels the extra prologue cost 0.7 % of the flagship's time
-// with count mode off, and count mode gained nothing at small_vocab.
+// loss_sum), which saves that launch for a short batch. The fp32 resident kernel (before
+// its first row) and the bf16 kernels with two row buffers (behind their first row's loads)
+// take this path; in the single-buffer bf16 kernels the extra prologue cost 0.7 % of the
+// flagship's time even with count mode off. Counting behind the first row's loads in the
+// fp32 kernel too was measured slower (the tiny batch's step 27.5 us against 25.6 us).
 template <int NT>
 __device__ float call_scale(const RowArgs& a) {
   if (a.mode == kModeLogprob) return 1.0f;
