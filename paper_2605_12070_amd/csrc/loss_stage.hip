@@ -1450,7 +1450,7 @@ constexpr bool kF32Persistent[kNumResident] = {true,  true,  true,  true,  true,
 // 27) and 30 for 1024 x 12 and 19 (6 %, 3 %); the long-row prefix kernels at 31 (bf16, 6 %)
 // and 32 (fp32, 2 %). The bf16 backward 512 x 8 shape is set for the small_vocab batch
 // (T = 4096, count mode): 31 gives a 1.4-1.7 % shorter step than 29 (27: 1.6 % longer, 30:
-// 0.3 % shorter, 32: 0.3 % shorter; each in two same-process runs), the same time at
+// 0.6 % shorter, 32: 0.3 % shorter; same-process runs), the same time at
 // T = 16384, 0.3-0.5 % less at T = 8192 and 1-2 % more at T = 2048.
 // Shapes:                                   256x1 256x2 256x4 512x4 512x6 512x8 1Kx6 1Kx8 1Kx12 1Kx19
 constexpr int kFillBf16Bwd[kNumResident] = {27,   27,   27,   32,   29,   31,   27,  27,  29,   27};
